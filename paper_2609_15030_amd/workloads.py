@@ -38,11 +38,16 @@ BF16 = "bf16"
 
 
 def round_to_bf16(x: np.ndarray) -> np.ndarray:
-    """Round an array to bf16 (nearest even) and return it as float32."""
-    x32 = np.ascontiguousarray(x, dtype=np.float32)
-    u = x32.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return (u.astype(np.uint32) << 16).view(np.float32)
+    """Round a finite array to bf16 (nearest even) and return it as float32.
+
+    Works on the fp32 bit pattern: add 0x7FFF plus the lowest kept bit, then
+    clear the 16 dropped bits (no overflow for finite values)."""
+    u = np.array(x, dtype=np.float32, copy=True).view(np.uint32)
+    lsb = (u >> 16) & 1
+    u += np.uint32(0x7FFF)
+    u += lsb
+    u &= np.uint32(0xFFFF0000)
+    return u.view(np.float32)
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -114,24 +119,37 @@ class Inputs:
                       self.cu_seqlens.copy(), self.io_dtype)
 
 
+def _normals(rng, shape, io_dtype, unit_rows):
+    """N(0,1) draws in fp64, optionally L2-normalised per last-axis row, then
+    rounded to the storage dtype.  Drawn in blocks of rows (the block size
+    does not change the values: PCG64 fills arrays in C order)."""
+    T = shape[0]
+    out = np.empty(shape, np.float32)
+    step = max(1, (1 << 22) // int(np.prod(shape[1:])))
+    for a in range(0, T, step):
+        b = min(T, a + step)
+        x = rng.standard_normal((b - a,) + tuple(shape[1:]))
+        if unit_rows:
+            x /= np.linalg.norm(x, axis=-1, keepdims=True)
+        out[a:b] = _store(x, io_dtype)
+    return out
+
+
 def draw(rng: np.random.Generator, seqlens, n_heads: int, dk: int, dv: int,
          io_dtype: str) -> Inputs:
     """Draw one packed input with the distributions stated in the module doc."""
     seqlens = [int(n) for n in seqlens]
     T = int(sum(seqlens))
-    q = rng.standard_normal((T, n_heads, dk))
-    q /= np.linalg.norm(q, axis=-1, keepdims=True)
-    k = rng.standard_normal((T, n_heads, dk))
-    k /= np.linalg.norm(k, axis=-1, keepdims=True)
-    v = rng.standard_normal((T, n_heads, dv))
+    q = _normals(rng, (T, n_heads, dk), io_dtype, True)
+    k = _normals(rng, (T, n_heads, dk), io_dtype, True)
+    v = _normals(rng, (T, n_heads, dv), io_dtype, False)
     b_logit = rng.standard_normal((T, n_heads))
     g_logit = rng.standard_normal((T, n_heads))
     beta = (1.0 / (1.0 + np.exp(-b_logit))).astype(np.float32)
     g = (-np.logaddexp(0.0, g_logit)).astype(np.float32)
     cu = np.zeros(len(seqlens) + 1, np.int32)
     cu[1:] = np.cumsum(seqlens)
-    return Inputs(_store(q, io_dtype), _store(k, io_dtype), _store(v, io_dtype),
-                  g, beta, cu, io_dtype)
+    return Inputs(q, k, v, g, beta, cu, io_dtype)
 
 
 def random_inputs(seed: int, seqlens, n_heads: int, dk: int, dv: int,
@@ -212,10 +230,13 @@ VARLEN_POOL_PAGES = 4096
 VARLEN_CKPT_SLOTS = 32          # 8,192 / 256 checkpoint slots per sequence
 
 
-def batched_varlen() -> Workload:
+def batched_varlen(with_data: bool = True) -> Workload:
     """16 sequences, lengths uniform in [1024, 8192] rounded down to 16,
     8 heads, d = 128, bf16, C = 256, with a 4,096-page pool addressed through
-    a random permutation page table, and a per-sequence restore mode."""
+    a random permutation page table, and a per-sequence restore mode.
+
+    ``with_data=False`` skips the tensor draw (inputs hold 0-token arrays but
+    the true cu_seqlens); the metadata does not depend on it."""
     root = np.random.SeedSequence(4)
     data_ss, meta_ss = root.spawn(2)
     meta = _gen(meta_ss)
@@ -229,7 +250,11 @@ def batched_varlen() -> Workload:
         kept.append(int(meta.integers(0, usable)) if mode == "partial" else
                     (usable if mode == "complete" else 0))
     perm = meta.permutation(VARLEN_POOL_PAGES).astype(np.int32)
-    x = draw(_gen(data_ss), lens, 8, 128, 128, BF16)
+    if with_data:
+        x = draw(_gen(data_ss), lens, 8, 128, 128, BF16)
+    else:
+        x = draw(_gen(data_ss), [0], 8, 128, 128, BF16)
+        x.cu_seqlens = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
     available = [k * C if m != "complete" else n
                  for n, m, k in zip(lens, modes, kept)]
     return Workload("varlen16_H8_d128_bf16_C256", x, interval=C,
