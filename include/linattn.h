@@ -1,0 +1,206 @@
+/*
+ * linattn.h - strict-prefix linear-attention prefill for one tensor-parallel
+ * rank's heads on one MI355X (gfx950).
+ *
+ * C ABI.  Every buffer is a plain pointer; "device" pointers are HIP device
+ * memory on the current device, "host" pointers are ordinary host memory.
+ * Streams and events are passed as void* (a hipStream_t / hipEvent_t; NULL
+ * stream = the null stream).  No C++ exception crosses this boundary.
+ *
+ * Notation follows the paper (section 2.2, "State position and scheduler
+ * position"): N is a prompt length, C the checkpoint interval (the paper's
+ * cache block, Table 1), B the prefix a restored state represents and p the
+ * scheduler's computed-token count.  Prefix lengths are counts and token
+ * indices are zero based; a state for prefix [0, B) continues from B.
+ *
+ * The recurrence is the gated delta rule (the paper names Flash Linear
+ * Attention kernels but does not write it out; the form below is the one the
+ * library is specified with).  Per sequence and head, with state S (dk x dv):
+ *
+ *   LA_GDR_LITERAL:        S_t = exp(g_t) S_{t-1} + beta_t k_t (v_t - S_{t-1}^T k_t)^T
+ *   LA_GDR_DECAYED_DELTA:  S_t = exp(g_t) S_{t-1} + beta_t k_t (v_t - exp(g_t) S_{t-1}^T k_t)^T
+ *   o_t = scale * S_t^T q_t
+ *
+ * Data layout ("packed varlen"): the tokens of all sequences are
+ * concatenated; sequence i owns rows cu_seqlens[i] .. cu_seqlens[i+1]-1.
+ *   q, k   [T_total, H, dk]   io dtype (bf16 or fp32), row-major
+ *   v, o   [T_total, H, dv]   io dtype
+ *   g, beta[T_total, H]       fp32 (g <= 0 keeps every exponent <= 0; not checked)
+ *   states [n, H, dk, dv]     fp32 (recurrent state, checkpoints, final state)
+ * q, k, v, o, states and the workspace must be 16-byte aligned.
+ *
+ * Errors: a problem visible on the host (shape, dtype, alignment, an empty
+ * suffix, a misaligned restored state, a short workspace) returns a status
+ * before anything is launched and leaves every output untouched.  A failed
+ * launch returns LA_ERR_HIP; la_last_error_message() then describes it.
+ * All work is queued on the given stream in order; nothing synchronises the
+ * host.  Outputs must not alias inputs.  The library allocates nothing and
+ * keeps no pointer after a call returns.
+ */
+#ifndef LINATTN_H
+#define LINATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum la_status {
+    LA_OK = 0,
+    LA_ERR_INVALID_ARG = 1,       /* null/misaligned pointer, bad size, bad table      */
+    LA_ERR_UNSUPPORTED = 2,       /* valid but not built: head dims, chunk size         */
+    LA_ERR_EMPTY_SUFFIX = 3,      /* resume with B_i == N_i (nothing to schedule)       */
+    LA_ERR_MISALIGNED_STATE = 4,  /* resume with B_i not a multiple of C                */
+    LA_ERR_HIP = 5,               /* HIP runtime reported an error                      */
+    LA_ERR_WORKSPACE = 6          /* workspace smaller than la_prefill_workspace_bytes  */
+} la_status;
+
+typedef enum la_dtype { LA_F32 = 0, LA_BF16 = 1 } la_dtype;
+
+typedef enum la_variant {
+    LA_GDR_LITERAL = 0,           /* prediction S_{t-1}^T k_t                 */
+    LA_GDR_DECAYED_DELTA = 1      /* prediction exp(g_t) S_{t-1}^T k_t        */
+} la_variant;
+
+/* Problem shape shared by the prefill entry points. */
+typedef struct la_shape {
+    int32_t n_seqs;          /* >= 1                                                 */
+    int32_t n_heads;         /* H >= 1: this rank's heads                            */
+    int32_t dk, dv;          /* head dims; built: dk, dv in {64, 128}                */
+    int32_t chunk;           /* tokens per chunk; built: 64                          */
+    int32_t ckpt_interval;   /* C >= 1: checkpoints at absolute multiples of C       */
+    int32_t io_dtype;        /* la_dtype of q, k, v, o                               */
+    int32_t variant;         /* la_variant                                           */
+    float scale;             /* output scale (1.0 in the paper's setting)            */
+} la_shape;
+
+/*
+ * strict_prefix_boundary - the repaired lookup rule (paper, section 2.2 and
+ * section 3.2; the worked examples of Table 4).
+ *
+ * Restricting the lookup to the prompt without its last token selects
+ * B = C * floor((N - 1) / C); the scheduler then computes the nonempty
+ * suffix [B, N).  In a general cache the checkpoint must also be available:
+ * with a contiguous cached prefix of `available_tokens` tokens,
+ *     B = min(C * floor((N - 1) / C), C * floor(available_tokens / C)).
+ * B = 0 means a cold start.  Writes B to *boundary_out.
+ * Errors: LA_ERR_INVALID_ARG if n_tokens < 1, interval < 1,
+ * available_tokens < 0 or boundary_out is NULL (nothing is written).
+ * Host only; touches no device.
+ */
+la_status strict_prefix_boundary(int64_t n_tokens, int64_t interval,
+                                 int64_t available_tokens, int64_t *boundary_out);
+
+/*
+ * la_prefill_workspace_bytes - size of the device workspace la_prefill and
+ * la_prefill_resume need for `total_tokens` tokens over shape->n_seqs
+ * sequences.  Returns 0 for an invalid or unsupported shape.  Host only.
+ */
+size_t la_prefill_workspace_bytes(const la_shape *shape, int64_t total_tokens);
+
+/*
+ * la_prefill - cold chunked prefill, the computation a cold recomputation
+ * runs (paper, sections 2.2 and 5.5), emitting fp32 state checkpoints at
+ * cache-block boundaries (the matched checkpoint schedule of section 4).
+ *
+ * Sequence i covers absolute positions [0, N_i) with N_i = cu[i+1] - cu[i]
+ * (N_i = 0 is allowed: no output rows, zero final state).
+ *   q, k, v, g, beta, o   device, layouts above
+ *   cu_seqlens_dev/host   int32 [n_seqs + 1], same values on both sides;
+ *                         cu[0] = 0, non-decreasing (host copy is validated)
+ *   final_state           device fp32 [n_seqs, H, dk, dv] or NULL
+ *   ckpt_out              device fp32 [rows, H, dk, dv] or NULL.  The state
+ *                         for prefix [0, P) at every P = j*C <= N_i goes to
+ *                         row ckpt_offsets[i] + (j - 1).
+ *   ckpt_offsets_dev/host int32 [n_seqs] row offsets (required iff ckpt_out)
+ *   workspace, ws_bytes   device scratch of la_prefill_workspace_bytes()
+ *   stream                hipStream_t
+ */
+la_status la_prefill(const la_shape *shape,
+                     const void *q, const void *k, const void *v,
+                     const float *g, const float *beta,
+                     const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                     void *o, float *final_state,
+                     float *ckpt_out, const int32_t *ckpt_offsets_dev,
+                     const int32_t *ckpt_offsets_host,
+                     void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * la_prefill_resume - continue from restored states (paper, section 2.2:
+ * computed = B, scheduled = N - B; section 5.2 reports exactly this first
+ * batch after the repair).
+ *
+ * The token arrays hold only the suffixes: sequence i's rows are the tokens
+ * at absolute positions [B_i, N_i), with N_i - B_i = cu[i+1] - cu[i].
+ *   start_pos_dev/host  int64 [n_seqs]: B_i, the prefix the restored state
+ *                       represents AND the position of the first scheduled
+ *                       token (one number, so the two cannot disagree).
+ *   state_in            device fp32 [n_seqs, H, dk, dv]: the state for prefix
+ *                       [0, B_i) (zeros where B_i = 0).
+ * Checkpoints are those at P = j*C with B_i < P <= N_i, to rows
+ * ckpt_offsets[i] + (j - B_i / C - 1).  Other arguments as la_prefill.
+ * Errors: LA_ERR_EMPTY_SUFFIX if some N_i - B_i == 0 (the pre-fix failure of
+ * section 3.2 needs exactly such a call); LA_ERR_MISALIGNED_STATE if some
+ * B_i is not a multiple of C (no checkpoint represents that prefix).
+ */
+la_status la_prefill_resume(const la_shape *shape,
+                            const void *q, const void *k, const void *v,
+                            const float *g, const float *beta,
+                            const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                            const int64_t *start_pos_dev, const int64_t *start_pos_host,
+                            const float *state_in,
+                            void *o, float *final_state,
+                            float *ckpt_out, const int32_t *ckpt_offsets_dev,
+                            const int32_t *ckpt_offsets_host,
+                            void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * la_state_save_paged - scatter states into a paged fp32 pool (the paper's
+ * page rows, section 3.1 and Table 5; a save must complete before dependent
+ * reuse, so order the reuse on the same stream or behind an event).
+ *
+ * Item n of `states` ([n_items, page_elems] fp32, device) goes to
+ * pool page page_ids[n] ([n_pages, page_elems] fp32, device).  Id -1 skips
+ * the item; any other id outside [0, n_pages) skips it and increments
+ * *err_count_dev (device int32, may be NULL).  Duplicate destination ids in
+ * one call are a caller error (unspecified winner).  page_elems must be a
+ * positive multiple of 4; states and pool 16-byte aligned.
+ */
+la_status la_state_save_paged(const float *states, int64_t n_items, int64_t page_elems,
+                              float *pool, int64_t n_pages, const int32_t *page_ids_dev,
+                              int32_t *err_count_dev, void *stream);
+
+/*
+ * la_state_restore_paged - gather states from the pool (the reload of
+ * section 3.2 / 5.5).  states[n] = pool[page_ids[n]]; id -1 writes a zero
+ * state (cold start); any other out-of-range id leaves states[n] untouched
+ * and increments *err_count_dev.  Sizes and alignment as the save.
+ */
+la_status la_state_restore_paged(const float *pool, int64_t n_pages,
+                                 const int32_t *page_ids_dev, float *states,
+                                 int64_t n_items, int64_t page_elems,
+                                 int32_t *err_count_dev, void *stream);
+
+/* Name of a status code (static string). */
+const char *la_status_string(la_status status);
+
+/* Description of the last error returned on this thread (static per thread). */
+const char *la_last_error_message(void);
+
+/*
+ * la_trace_set_events - profiling hook.  When `events` holds at least 4
+ * hipEvent_t (created by the caller), every later la_prefill /
+ * la_prefill_resume call on this thread records events[0] before its first
+ * kernel, events[1] after the chunk-preparation kernel, events[2] after the
+ * inter-chunk scan kernel and events[3] after the output kernel, all on the
+ * call's stream.  n_events = 0 (or events = NULL) switches it off.
+ */
+void la_trace_set_events(void *const *events, int32_t n_events);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LINATTN_H */

@@ -1,0 +1,141 @@
+// Device helpers shared by the gfx950 kernels: MFMA traits, fragment
+// layouts, and the chunk plan (which tokens form which chunk, where a
+// chunk's intermediates live in the workspace).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace la {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kChunk = 64;        // rows of one chunk tile (the prefill's chunk size)
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// MFMA traits.  One 16x16 output tile per instruction, fp32 accumulation.
+//   bf16: v_mfma_f32_16x16x32_bf16, 8 operand values per lane and k-step.
+//   fp32: v_mfma_f32_16x16x4_f32,   1 operand value per lane and k-step.
+// Lane layout (lane l, g = l / 16):
+//   A (16 x KSTEP): row l % 16, k = g * KW + j   (j < KW)
+//   B (KSTEP x 16): col l % 16, k = g * KW + j
+//   C (16 x 16):    col l % 16, rows 4 * g + i   (i < 4)
+// ---------------------------------------------------------------------------
+template <typename T> struct MT;
+
+template <> struct MT<__bf16> {
+    static constexpr int KW = 8;
+    static constexpr int KSTEP = 32;
+    typedef bf16x8 frag;
+    __device__ static inline f32x4 mma(frag a, frag b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+    // 8 consecutive values; v must be 16-byte aligned.
+    __device__ static inline frag pack(const __bf16 *v) { return *(const frag *)v; }
+    // Two runs of 4 consecutive values (8-byte aligned each).
+    __device__ static inline frag pack2(const __bf16 *lo, const __bf16 *hi) {
+        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+        const bf16x4 a = *(const bf16x4 *)lo, b = *(const bf16x4 *)hi;
+        return frag{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    }
+};
+
+template <> struct MT<float> {
+    static constexpr int KW = 1;
+    static constexpr int KSTEP = 4;
+    typedef float frag;
+    __device__ static inline f32x4 mma(frag a, frag b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+    __device__ static inline frag pack(const float *v) { return v[0]; }
+    __device__ static inline frag pack2(const float *lo, const float *) { return lo[0]; }
+};
+
+template <typename T> __device__ inline T from_f32(float x);
+template <> __device__ inline float from_f32<float>(float x) { return x; }
+template <> __device__ inline __bf16 from_f32<__bf16>(float x) { return (__bf16)x; }  // RNE
+
+template <typename T> __device__ inline float to_f32(T x) { return (float)x; }
+
+// Elements of T per 16-byte vector.
+template <typename T> struct Vec { static constexpr int N = 16 / sizeof(T); };
+
+__device__ inline f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+// Contraction-index permutation.  When the B operand of a product is taken
+// straight from a C-layout accumulator (rows 4g+i of each 16-row tile held
+// by lane group g), the lane's flat operand index f (f = ks*KW + j over all
+// k-steps) stands for accumulator row perm_row(f, g).  The A operand of the
+// same product is then loaded at those rows, so no cross-lane shuffle of the
+// accumulator is needed.  Every row of the tile set is hit exactly once per
+// k-step group, and each k-step covers KSTEP distinct rows.
+__device__ __host__ inline int perm_row(int f, int g) {
+    return 16 * (f >> 2) + 4 * g + (f & 3);
+}
+
+// ---------------------------------------------------------------------------
+// Chunk plan.  A sequence's call covers local positions [0, len) starting at
+// an absolute position that is a multiple of C.  Chunks never straddle a
+// checkpoint position: each C-token segment is cut into ceil(C / 64) chunks
+// of at most 64 tokens, so every checkpoint falls on a chunk end.  With C a
+// multiple of 64 this is the plain 64-token grid.
+// ---------------------------------------------------------------------------
+__device__ __host__ inline int chunks_per_interval(int C) { return (C + kChunk - 1) / kChunk; }
+
+__device__ __host__ inline int64_t n_chunks(int64_t len, int64_t C, int cps) {
+    const int64_t full = len / C, rem = len % C;
+    return full * cps + (rem + kChunk - 1) / kChunk;
+}
+
+// Local token range [a, b) of chunk j.
+__device__ __host__ inline void chunk_range(int64_t j, int64_t len, int64_t C, int cps,
+                                            int64_t *a, int64_t *b) {
+    const int64_t seg = j / cps, sub = j % cps;
+    const int64_t lo = seg * C + (int64_t)sub * kChunk;
+    int64_t hi = lo + kChunk;
+    if (hi > (seg + 1) * C) hi = (seg + 1) * C;
+    if (hi > len) hi = len;
+    *a = lo;
+    *b = hi;
+}
+
+// First workspace slot of sequence i.  A sequence of n tokens has at most
+// ceil(n * cps / C) chunks, so slot bases floor((cu[i] * cps + (C - 1) * i) / C)
+// give every sequence room for its chunks without a prefix sum over the
+// batch: the difference of consecutive bases is at least ceil(n_i * cps / C).
+__device__ __host__ inline int64_t slot_base(int64_t cu_i, int64_t i, int64_t C, int cps) {
+    return (cu_i * cps + (C - 1) * i) / C;
+}
+
+__device__ __host__ inline int64_t total_slots(int64_t total_tokens, int64_t n_seqs, int64_t C,
+                                               int cps) {
+    return slot_base(total_tokens, n_seqs, C, cps);
+}
+
+// ---------------------------------------------------------------------------
+// Workspace regions (per slot and head), all produced and consumed on the
+// device within one prefill call.
+//   W   : -W in A-operand order for the state contraction      [4][DK/4] x 64 lanes, io type
+//   KT  : decayed keys^T in A-operand order (chunk rows perm.) [DK/16][16] x 64 lanes, io type
+//   UT  : U~ = T diag(beta) V, C-layout per 16x16 tile        [DV/16][4] x 64 lanes x 4, fp32
+//   G   : chunk-local cumulative gate                          [64], fp32
+//   SC  : state entering the chunk, B-operand order            [DV/16][DK/4] x 64 lanes, io type
+//   U   : U = U~ - W S, B-operand order                        [DV/16][16] x 64 lanes, io type
+// ---------------------------------------------------------------------------
+struct Workspace {
+    void *w, *kt, *sc, *u;
+    float *ut, *g;
+};
+
+template <typename T, int DK, int DV> struct WsLayout {
+    static constexpr size_t w_elems = (size_t)kChunk * DK;      // per slot-head
+    static constexpr size_t kt_elems = (size_t)DK * kChunk;
+    static constexpr size_t ut_elems = (size_t)kChunk * DV;
+    static constexpr size_t g_elems = kChunk;
+    static constexpr size_t sc_elems = (size_t)DK * DV;
+    static constexpr size_t u_elems = (size_t)kChunk * DV;
+};
+
+}  // namespace la

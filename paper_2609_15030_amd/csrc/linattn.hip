@@ -1,0 +1,325 @@
+// C ABI of the strict-prefix linear-attention prefill library (gfx950).
+// Host side: argument validation, the chunk plan's sizes, workspace carving
+// and launches.  Kernels live in the headers included below.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "linattn.h"
+#include "la_common.h"
+#include "gdr_prep.h"
+#include "gdr_scan.h"
+#include "gdr_out.h"
+#include "paged.h"
+
+namespace {
+
+thread_local char g_msg[512] = "";
+thread_local void *g_trace[4] = {nullptr, nullptr, nullptr, nullptr};
+thread_local int g_trace_n = 0;
+
+la_status fail(la_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_msg, sizeof(g_msg), fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+la_status hip_check(const char *what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(LA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return LA_OK;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+constexpr int kScanBV = 16;       // state columns per scan wave
+constexpr size_t kRegionAlign = 256;
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+size_t io_size(int32_t dtype) { return dtype == LA_BF16 ? 2 : 4; }
+
+bool shape_supported(const la_shape *s) {
+    return (s->dk == 64 || s->dk == 128) && (s->dv == 64 || s->dv == 128) && s->chunk == la::kChunk;
+}
+
+la_status check_shape(const la_shape *s) {
+    if (!s) return fail(LA_ERR_INVALID_ARG, "shape is NULL");
+    if (s->n_seqs < 1 || s->n_seqs > 65535) return fail(LA_ERR_INVALID_ARG, "n_seqs=%d outside [1, 65535]", s->n_seqs);
+    if (s->n_heads < 1 || s->n_heads > 65535) return fail(LA_ERR_INVALID_ARG, "n_heads=%d outside [1, 65535]", s->n_heads);
+    if (s->ckpt_interval < 1) return fail(LA_ERR_INVALID_ARG, "ckpt_interval=%d < 1", s->ckpt_interval);
+    if (s->io_dtype != LA_F32 && s->io_dtype != LA_BF16) return fail(LA_ERR_INVALID_ARG, "io_dtype=%d", s->io_dtype);
+    if (s->variant != LA_GDR_LITERAL && s->variant != LA_GDR_DECAYED_DELTA)
+        return fail(LA_ERR_INVALID_ARG, "variant=%d", s->variant);
+    if (!std::isfinite(s->scale)) return fail(LA_ERR_INVALID_ARG, "scale is not finite");
+    if (s->dk < 1 || s->dv < 1 || s->chunk < 1) return fail(LA_ERR_INVALID_ARG, "dk, dv, chunk must be >= 1");
+    if (!shape_supported(s))
+        return fail(LA_ERR_UNSUPPORTED, "dk=%d dv=%d chunk=%d not built (dk, dv in {64, 128}, chunk 64)",
+                    s->dk, s->dv, s->chunk);
+    return LA_OK;
+}
+
+struct WsPlan {
+    size_t w, kt, ut, g, sc, u, total;   // byte offsets of each region, total size
+};
+
+WsPlan plan_workspace(const la_shape *s, int64_t total_tokens) {
+    const int cps = la::chunks_per_interval(s->ckpt_interval);
+    const int64_t slots = la::total_slots(total_tokens, s->n_seqs, s->ckpt_interval, cps);
+    const size_t sh = (size_t)slots * s->n_heads;
+    const size_t io = io_size(s->io_dtype);
+    WsPlan p;
+    size_t off = 0;
+    auto take = [&](size_t bytes) { const size_t at = off; off = round_up(off + bytes, kRegionAlign); return at; };
+    p.w = take(sh * la::kChunk * s->dk * io);
+    p.kt = take(sh * s->dk * la::kChunk * io);
+    p.ut = take(sh * la::kChunk * s->dv * sizeof(float));
+    p.g = take(sh * la::kChunk * sizeof(float));
+    p.sc = take(sh * (size_t)s->dk * s->dv * io);
+    p.u = take(sh * la::kChunk * s->dv * io);
+    p.total = std::max<size_t>(off, kRegionAlign);
+    return p;
+}
+
+struct PrefillCall {
+    const la_shape *shape;
+    const void *q, *k, *v;
+    const float *g, *beta;
+    const int32_t *cu_dev, *cu_host;
+    const int64_t *start_dev, *start_host;   // null for a cold prefill
+    const float *state_in;                   // null for a cold prefill
+    void *o;
+    float *final_state, *ckpt_out;
+    const int32_t *ckpt_off_dev, *ckpt_off_host;
+    void *workspace;
+    size_t ws_bytes;
+    hipStream_t stream;
+};
+
+template <typename T, int DK, int DV>
+la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) {
+    const la_shape *s = c.shape;
+    const int cps = la::chunks_per_interval(s->ckpt_interval);
+    char *base = (char *)c.workspace;
+    la::Workspace ws;
+    ws.w = base + p.w;
+    ws.kt = base + p.kt;
+    ws.ut = (float *)(base + p.ut);
+    ws.g = (float *)(base + p.g);
+    ws.sc = base + p.sc;
+    ws.u = base + p.u;
+
+    const bool trace = g_trace_n >= 4;
+    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[0], c.stream);
+    (void)hipGetLastError();
+
+    if (max_chunks > 0) {
+        la::PrepArgs pa{c.k, c.v, c.g, c.beta, c.cu_dev, s->n_heads, s->ckpt_interval, cps, s->variant, ws};
+        dim3 grid((unsigned)max_chunks, (unsigned)s->n_heads, (unsigned)s->n_seqs);
+        hipLaunchKernelGGL((la::gdr_prep_kernel<T, DK, DV>), grid, dim3(256), 0, c.stream, pa);
+        if (la_status e = hip_check("chunk preparation launch")) return e;
+    }
+    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[1], c.stream);
+    {
+        la::ScanArgs sa{c.cu_dev, c.state_in, c.final_state, c.ckpt_out, c.ckpt_off_dev,
+                        s->n_seqs, s->n_heads, s->ckpt_interval, cps, ws};
+        constexpr int NT = DV / kScanBV;
+        const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
+        const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
+        hipLaunchKernelGGL((la::gdr_scan_kernel<T, DK, DV, kScanBV>), dim3((unsigned)blocks), dim3(64), 0,
+                           c.stream, sa);
+        if (la_status e = hip_check("inter-chunk scan launch")) return e;
+    }
+    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[2], c.stream);
+    if (max_chunks > 0) {
+        la::OutArgs oa{c.q, c.k, c.o, c.cu_dev, s->n_heads, s->ckpt_interval, cps, s->scale, ws};
+        dim3 grid((unsigned)max_chunks, (unsigned)s->n_heads, (unsigned)s->n_seqs);
+        hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), grid, dim3(256), 0, c.stream, oa);
+        if (la_status e = hip_check("output launch")) return e;
+    }
+    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[3], c.stream);
+    return LA_OK;
+}
+
+template <typename T>
+la_status dispatch_dims(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) {
+    const int dk = c.shape->dk, dv = c.shape->dv;
+    if (dk == 64 && dv == 64) return launch_prefill<T, 64, 64>(c, p, max_chunks);
+    if (dk == 64 && dv == 128) return launch_prefill<T, 64, 128>(c, p, max_chunks);
+    if (dk == 128 && dv == 64) return launch_prefill<T, 128, 64>(c, p, max_chunks);
+    if (dk == 128 && dv == 128) return launch_prefill<T, 128, 128>(c, p, max_chunks);
+    return fail(LA_ERR_UNSUPPORTED, "dk=%d dv=%d", dk, dv);
+}
+
+la_status run_prefill(const PrefillCall &c) {
+    if (la_status e = check_shape(c.shape)) return e;
+    const la_shape *s = c.shape;
+    const bool resume = c.start_host != nullptr || c.start_dev != nullptr;
+    const int64_t C = s->ckpt_interval;
+    const int cps = la::chunks_per_interval(s->ckpt_interval);
+
+    if (!c.cu_dev || !c.cu_host) return fail(LA_ERR_INVALID_ARG, "cu_seqlens_dev and cu_seqlens_host are required");
+    if (c.cu_host[0] != 0) return fail(LA_ERR_INVALID_ARG, "cu_seqlens[0]=%d, must be 0", c.cu_host[0]);
+    int64_t max_chunks = 0;
+    for (int i = 0; i < s->n_seqs; ++i) {
+        const int64_t len = (int64_t)c.cu_host[i + 1] - c.cu_host[i];
+        if (len < 0) return fail(LA_ERR_INVALID_ARG, "cu_seqlens decreases at sequence %d", i);
+        max_chunks = std::max(max_chunks, la::n_chunks(len, C, cps));
+    }
+    const int64_t total = c.cu_host[s->n_seqs];
+    if (resume) {
+        if (!c.start_host || !c.start_dev) return fail(LA_ERR_INVALID_ARG, "start_pos_dev and start_pos_host are required");
+        if (!c.state_in) return fail(LA_ERR_INVALID_ARG, "state_in is required for a resume");
+        for (int i = 0; i < s->n_seqs; ++i) {
+            const int64_t B = c.start_host[i];
+            const int64_t len = (int64_t)c.cu_host[i + 1] - c.cu_host[i];
+            if (B < 0) return fail(LA_ERR_INVALID_ARG, "start_pos[%d]=%lld < 0", i, (long long)B);
+            if (B % C != 0)
+                return fail(LA_ERR_MISALIGNED_STATE, "start_pos[%d]=%lld is not a multiple of C=%lld: no checkpoint "
+                            "represents that prefix", i, (long long)B, (long long)C);
+            if (len == 0)
+                return fail(LA_ERR_EMPTY_SUFFIX, "sequence %d has an empty suffix (B = N = %lld): the restored state "
+                            "already covers the prompt", i, (long long)B);
+            if (B > ((int64_t)1 << 40)) return fail(LA_ERR_INVALID_ARG, "start_pos[%d] too large", i);
+        }
+    }
+    if (max_chunks > 0x7fffffff) return fail(LA_ERR_INVALID_ARG, "sequence too long");
+    if (total > 0) {
+        if (!c.q || !c.k || !c.v || !c.g || !c.beta || !c.o)
+            return fail(LA_ERR_INVALID_ARG, "q, k, v, g, beta and o are required");
+        if (!aligned16(c.q) || !aligned16(c.k) || !aligned16(c.v) || !aligned16(c.o))
+            return fail(LA_ERR_INVALID_ARG, "q, k, v and o must be 16-byte aligned");
+    }
+    if (c.state_in && !aligned16(c.state_in)) return fail(LA_ERR_INVALID_ARG, "state_in must be 16-byte aligned");
+    if (c.final_state && !aligned16(c.final_state)) return fail(LA_ERR_INVALID_ARG, "final_state must be 16-byte aligned");
+    if (c.ckpt_out) {
+        if (!aligned16(c.ckpt_out)) return fail(LA_ERR_INVALID_ARG, "ckpt_out must be 16-byte aligned");
+        if (!c.ckpt_off_dev || !c.ckpt_off_host)
+            return fail(LA_ERR_INVALID_ARG, "ckpt_offsets_dev and ckpt_offsets_host are required with ckpt_out");
+        for (int i = 0; i < s->n_seqs; ++i)
+            if (c.ckpt_off_host[i] < 0) return fail(LA_ERR_INVALID_ARG, "ckpt_offsets[%d] < 0", i);
+    }
+    const WsPlan p = plan_workspace(s, total);
+    if (!c.workspace || c.ws_bytes < p.total)
+        return fail(LA_ERR_WORKSPACE, "workspace of %zu bytes, %zu required", c.workspace ? c.ws_bytes : 0, p.total);
+    if (!aligned16(c.workspace)) return fail(LA_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    // The chunk plan's slot bound, checked on the host before any launch.
+    const int64_t slots = la::total_slots(total, s->n_seqs, C, cps);
+    for (int i = 0; i < s->n_seqs; ++i) {
+        const int64_t len = (int64_t)c.cu_host[i + 1] - c.cu_host[i];
+        if (la::slot_base(c.cu_host[i], i, C, cps) + la::n_chunks(len, C, cps) > slots)
+            return fail(LA_ERR_INVALID_ARG, "internal: chunk plan exceeds its workspace at sequence %d", i);
+    }
+
+    if (s->io_dtype == LA_BF16) return dispatch_dims<__bf16>(c, p, max_chunks);
+    return dispatch_dims<float>(c, p, max_chunks);
+}
+
+la_status check_paged(const float *a, const float *b, int64_t n_items, int64_t page_elems, int64_t n_pages,
+                      const int32_t *ids) {
+    if (n_items < 0 || n_items > 0x7fffffff) return fail(LA_ERR_INVALID_ARG, "n_items=%lld", (long long)n_items);
+    if (page_elems <= 0 || page_elems % 4 != 0)
+        return fail(LA_ERR_INVALID_ARG, "page_elems=%lld must be a positive multiple of 4", (long long)page_elems);
+    if (n_pages < 0 || n_pages > 0x7fffffff) return fail(LA_ERR_INVALID_ARG, "n_pages=%lld", (long long)n_pages);
+    if (n_items > 0 && (!a || !b || !ids)) return fail(LA_ERR_INVALID_ARG, "states, pool and page_ids are required");
+    if (!aligned16(a) || !aligned16(b)) return fail(LA_ERR_INVALID_ARG, "states and pool must be 16-byte aligned");
+    return LA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+la_status strict_prefix_boundary(int64_t n_tokens, int64_t interval, int64_t available_tokens,
+                                 int64_t *boundary_out) {
+    if (!boundary_out) return fail(LA_ERR_INVALID_ARG, "boundary_out is NULL");
+    if (n_tokens < 1) return fail(LA_ERR_INVALID_ARG, "N=%lld < 1: no strict prefix", (long long)n_tokens);
+    if (interval < 1) return fail(LA_ERR_INVALID_ARG, "C=%lld < 1", (long long)interval);
+    if (available_tokens < 0) return fail(LA_ERR_INVALID_ARG, "available=%lld < 0", (long long)available_tokens);
+    const int64_t query = (n_tokens - 1) / interval * interval;      // exclude the last prompt token
+    const int64_t avail = available_tokens / interval * interval;    // only whole cached blocks
+    *boundary_out = std::min(query, avail);
+    return LA_OK;
+}
+
+size_t la_prefill_workspace_bytes(const la_shape *shape, int64_t total_tokens) {
+    if (check_shape(shape) != LA_OK || total_tokens < 0) return 0;
+    return plan_workspace(shape, total_tokens).total;
+}
+
+la_status la_prefill(const la_shape *shape, const void *q, const void *k, const void *v, const float *g,
+                     const float *beta, const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host, void *o,
+                     float *final_state, float *ckpt_out, const int32_t *ckpt_offsets_dev,
+                     const int32_t *ckpt_offsets_host, void *workspace, size_t ws_bytes, void *stream) {
+    PrefillCall c{shape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host, nullptr, nullptr, nullptr,
+                  o, final_state, ckpt_out, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
+                  (hipStream_t)stream};
+    return run_prefill(c);
+}
+
+la_status la_prefill_resume(const la_shape *shape, const void *q, const void *k, const void *v, const float *g,
+                            const float *beta, const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                            const int64_t *start_pos_dev, const int64_t *start_pos_host, const float *state_in,
+                            void *o, float *final_state, float *ckpt_out, const int32_t *ckpt_offsets_dev,
+                            const int32_t *ckpt_offsets_host, void *workspace, size_t ws_bytes, void *stream) {
+    if (!start_pos_dev || !start_pos_host)
+        return fail(LA_ERR_INVALID_ARG, "start_pos_dev and start_pos_host are required");
+    PrefillCall c{shape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host, start_pos_dev, start_pos_host,
+                  state_in, o, final_state, ckpt_out, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
+                  (hipStream_t)stream};
+    return run_prefill(c);
+}
+
+la_status la_state_save_paged(const float *states, int64_t n_items, int64_t page_elems, float *pool,
+                              int64_t n_pages, const int32_t *page_ids_dev, int32_t *err_count_dev, void *stream) {
+    if (la_status e = check_paged(states, pool, n_items, page_elems, n_pages, page_ids_dev)) return e;
+    if (n_items == 0) return LA_OK;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(la::page_save_kernel, dim3((unsigned)n_items), dim3(la::kPageThreads), 0,
+                       (hipStream_t)stream, (const la::f32x4 *)states, page_elems / 4, (la::f32x4 *)pool,
+                       n_pages, page_ids_dev, err_count_dev);
+    return hip_check("page save launch");
+}
+
+la_status la_state_restore_paged(const float *pool, int64_t n_pages, const int32_t *page_ids_dev, float *states,
+                                 int64_t n_items, int64_t page_elems, int32_t *err_count_dev, void *stream) {
+    if (la_status e = check_paged(states, pool, n_items, page_elems, n_pages, page_ids_dev)) return e;
+    if (n_items == 0) return LA_OK;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(la::page_restore_kernel, dim3((unsigned)n_items), dim3(la::kPageThreads), 0,
+                       (hipStream_t)stream, (const la::f32x4 *)pool, n_pages, page_ids_dev, (la::f32x4 *)states,
+                       page_elems / 4, err_count_dev);
+    return hip_check("page restore launch");
+}
+
+const char *la_status_string(la_status status) {
+    switch (status) {
+        case LA_OK: return "LA_OK";
+        case LA_ERR_INVALID_ARG: return "LA_ERR_INVALID_ARG";
+        case LA_ERR_UNSUPPORTED: return "LA_ERR_UNSUPPORTED";
+        case LA_ERR_EMPTY_SUFFIX: return "LA_ERR_EMPTY_SUFFIX";
+        case LA_ERR_MISALIGNED_STATE: return "LA_ERR_MISALIGNED_STATE";
+        case LA_ERR_HIP: return "LA_ERR_HIP";
+        case LA_ERR_WORKSPACE: return "LA_ERR_WORKSPACE";
+    }
+    return "LA_ERR_UNKNOWN";
+}
+
+const char *la_last_error_message(void) { return g_msg; }
+
+void la_trace_set_events(void *const *events, int32_t n_events) {
+    if (!events || n_events < 4) {
+        g_trace_n = 0;
+        return;
+    }
+    for (int i = 0; i < 4; ++i) g_trace[i] = events[i];
+    g_trace_n = 4;
+}
+
+}  // extern "C"

@@ -1,0 +1,216 @@
+"""Python binding of the C ABI in include/linattn.h.
+
+Argument marshalling only: torch tensors become device pointers, NumPy
+arrays become host pointers, the current torch stream becomes the hipStream_t.
+Every step of the computation runs in the gfx950 library; if the library is
+missing this module raises on import rather than falling back to anything.
+
+Function names and argument order follow the C entry points.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "liblinattn.so")
+
+LA_OK = 0
+LA_ERR_INVALID_ARG = 1
+LA_ERR_UNSUPPORTED = 2
+LA_ERR_EMPTY_SUFFIX = 3
+LA_ERR_MISALIGNED_STATE = 4
+LA_ERR_HIP = 5
+LA_ERR_WORKSPACE = 6
+
+LA_F32 = 0
+LA_BF16 = 1
+LA_GDR_LITERAL = 0
+LA_GDR_DECAYED_DELTA = 1
+
+EXPORTED = ("strict_prefix_boundary", "la_prefill_workspace_bytes", "la_prefill",
+            "la_prefill_resume", "la_state_save_paged", "la_state_restore_paged",
+            "la_status_string", "la_last_error_message", "la_trace_set_events")
+
+
+class LaShape(ctypes.Structure):
+    _fields_ = [("n_seqs", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("dk", ctypes.c_int32), ("dv", ctypes.c_int32),
+                ("chunk", ctypes.c_int32), ("ckpt_interval", ctypes.c_int32),
+                ("io_dtype", ctypes.c_int32), ("variant", ctypes.c_int32),
+                ("scale", ctypes.c_float)]
+
+
+def make_shape(n_seqs, n_heads, dk, dv, ckpt_interval, io_dtype=LA_BF16,
+               variant=LA_GDR_LITERAL, scale=1.0, chunk=64) -> LaShape:
+    return LaShape(n_seqs, n_heads, dk, dv, chunk, ckpt_interval, io_dtype, variant, scale)
+
+
+class LinAttnError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{status_string(status)}: {message}")
+        self.status = status
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2609_15030_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    SH = ctypes.POINTER(LaShape)
+    sig = {
+        "strict_prefix_boundary": ([I64, I64, I64, ctypes.POINTER(I64)], I32),
+        "la_prefill_workspace_bytes": ([SH, I64], SZ),
+        "la_prefill": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "la_prefill_resume": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "la_state_save_paged": ([P, I64, I64, P, I64, P, P, P], I32),
+        "la_state_restore_paged": ([P, I64, P, P, I64, I64, P, P], I32),
+        "la_status_string": ([I32], ctypes.c_char_p),
+        "la_last_error_message": ([], ctypes.c_char_p),
+        "la_trace_set_events": ([ctypes.POINTER(P), I32], None),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    return lib
+
+
+_lib = _load()
+
+
+def library() -> ctypes.CDLL:
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return _lib.la_status_string(status).decode()
+
+
+def last_error_message() -> str:
+    return _lib.la_last_error_message().decode()
+
+
+def _check(status: int):
+    if status != LA_OK:
+        raise LinAttnError(status, last_error_message())
+
+
+def _dptr(t) -> Optional[int]:
+    """Device pointer of a torch tensor (None stays NULL)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def _hptr(a, dtype) -> Optional[ctypes.c_void_p]:
+    """Host pointer of a NumPy array (converted to ``dtype``, kept alive by the caller)."""
+    if a is None:
+        return None
+    assert a.dtype == dtype and a.flags.c_contiguous
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+# ---------------------------------------------------------------------------
+# entry points (same names as the C ABI)
+# ---------------------------------------------------------------------------
+
+def strict_prefix_boundary(n_tokens: int, interval: int, available_tokens: int) -> int:
+    out = ctypes.c_int64(-1)
+    _check(_lib.strict_prefix_boundary(int(n_tokens), int(interval), int(available_tokens),
+                                       ctypes.byref(out)))
+    return out.value
+
+
+def strict_prefix_boundary_status(n_tokens: int, interval: int, available_tokens: int):
+    """(status, B) without raising; B is -1 when nothing was written."""
+    out = ctypes.c_int64(-1)
+    st = _lib.strict_prefix_boundary(int(n_tokens), int(interval), int(available_tokens),
+                                     ctypes.byref(out))
+    return st, out.value
+
+
+def la_prefill_workspace_bytes(shape: LaShape, total_tokens: int) -> int:
+    return _lib.la_prefill_workspace_bytes(ctypes.byref(shape), int(total_tokens))
+
+
+def la_prefill(shape: LaShape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host: np.ndarray,
+               o, final_state=None, ckpt_out=None, ckpt_offsets_dev=None,
+               ckpt_offsets_host: Optional[np.ndarray] = None, workspace=None, stream=None,
+               check: bool = True) -> int:
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.la_prefill(ctypes.byref(shape), _dptr(q), _dptr(k), _dptr(v), _dptr(g), _dptr(beta),
+                         _dptr(cu_seqlens_dev), _hptr(cu_seqlens_host, np.int32), _dptr(o),
+                         _dptr(final_state), _dptr(ckpt_out), _dptr(ckpt_offsets_dev),
+                         _hptr(ckpt_offsets_host, np.int32), _dptr(workspace), ws_bytes,
+                         _stream(stream))
+    if check:
+        _check(st)
+    return st
+
+
+def la_prefill_resume(shape: LaShape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host: np.ndarray,
+                      start_pos_dev, start_pos_host: np.ndarray, state_in, o, final_state=None,
+                      ckpt_out=None, ckpt_offsets_dev=None,
+                      ckpt_offsets_host: Optional[np.ndarray] = None, workspace=None, stream=None,
+                      check: bool = True) -> int:
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.la_prefill_resume(ctypes.byref(shape), _dptr(q), _dptr(k), _dptr(v), _dptr(g),
+                                _dptr(beta), _dptr(cu_seqlens_dev), _hptr(cu_seqlens_host, np.int32),
+                                _dptr(start_pos_dev), _hptr(start_pos_host, np.int64),
+                                _dptr(state_in), _dptr(o), _dptr(final_state), _dptr(ckpt_out),
+                                _dptr(ckpt_offsets_dev), _hptr(ckpt_offsets_host, np.int32),
+                                _dptr(workspace), ws_bytes, _stream(stream))
+    if check:
+        _check(st)
+    return st
+
+
+def la_state_save_paged(states, pool, page_ids_dev, err_count_dev=None, stream=None,
+                        check: bool = True) -> int:
+    n_pages = pool.shape[0]
+    page_elems = pool[0].numel() if n_pages else states[0].numel()
+    n_items = page_ids_dev.numel()
+    st = _lib.la_state_save_paged(_dptr(states), n_items, page_elems, _dptr(pool), n_pages,
+                                  _dptr(page_ids_dev), _dptr(err_count_dev), _stream(stream))
+    if check:
+        _check(st)
+    return st
+
+
+def la_state_restore_paged(pool, page_ids_dev, states, err_count_dev=None, stream=None,
+                           check: bool = True) -> int:
+    n_pages = pool.shape[0]
+    page_elems = pool[0].numel() if n_pages else states[0].numel()
+    n_items = page_ids_dev.numel()
+    st = _lib.la_state_restore_paged(_dptr(pool), n_pages, _dptr(page_ids_dev), _dptr(states),
+                                     n_items, page_elems, _dptr(err_count_dev), _stream(stream))
+    if check:
+        _check(st)
+    return st
+
+
+def la_trace_set_events(events: Sequence[int]):
+    """events: hipEvent_t handles (ints); an empty sequence switches tracing off."""
+    if not events:
+        _lib.la_trace_set_events(None, 0)
+        return
+    arr = (ctypes.c_void_p * len(events))(*events)
+    _lib.la_trace_set_events(arr, len(events))

@@ -1,0 +1,138 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and
+its host-only logic (the boundary rule, workspace sizing, argument
+validation that returns before any launch) is right.  No device is touched:
+device pointers passed here are dummies that validation never dereferences.
+"""
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from oracle.boundary import strict_prefix_boundary as brute_boundary
+from paper_2609_15030_amd import linattn as la
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "linattn.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert set(names) == set(la.EXPORTED)
+    out = subprocess.run(["nm", "-D", "--defined-only", la.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for n in names:
+        assert n in exported, n
+        assert hasattr(la.library(), n)
+
+
+def test_library_targets_gfx950_only():
+    """The offload bundle ids embedded in the built library name gfx950 only."""
+    data = open(la.LIB_PATH, "rb").read()
+    targets = set(re.findall(rb"amdgcn-amd-amdhsa-+(gfx\w+)", data))
+    assert targets == {b"gfx950"}
+
+
+def _rows(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return [l.split() for l in f if l.strip() and not l.startswith("#")]
+
+
+@pytest.mark.parametrize("row", _rows("table4_boundary_matrix.txt"), ids=lambda r: r[0])
+def test_library_boundary_reproduces_table4(row):
+    N, B_after, suffix = int(row[0]), int(row[4]), int(row[5])
+    assert la.strict_prefix_boundary(N, 1792, N) == B_after
+    assert N - B_after == suffix
+
+
+def test_library_boundary_matches_brute_force():
+    for C in list(range(1, 40)) + [64, 256, 1024, 1792]:
+        for N in list(range(1, 300)) + [3583, 3584, 3585, 5375, 5376, 5377, 32768]:
+            for avail in (0, 1, C - 1, C, 2 * C + 1, N - 1, N, N + C, 10 ** 6):
+                if avail < 0:
+                    continue
+                assert la.strict_prefix_boundary(N, C, avail) == brute_boundary(N, C, avail), (N, C, avail)
+
+
+def test_library_boundary_rejects_invalid():
+    for args in [(0, 16, 0), (-5, 16, 3), (10, 0, 10), (10, -2, 10), (10, 4, -1)]:
+        st, b = la.strict_prefix_boundary_status(*args)
+        assert st == la.LA_ERR_INVALID_ARG and b == -1
+    assert la.library().strict_prefix_boundary(10, 4, 10, None) == la.LA_ERR_INVALID_ARG
+
+
+def test_workspace_bytes():
+    sh = la.make_shape(1, 8, 128, 128, 256)
+    a = la.la_prefill_workspace_bytes(sh, 3584)
+    b = la.la_prefill_workspace_bytes(sh, 7168)
+    assert 0 < a < b
+    # 56 chunks x 8 heads x (W, K~^T, S_0, U in bf16; U~, G in fp32)
+    per = 64 * 128 * 2 * 2 + 64 * 128 * 4 + 64 * 4 + 128 * 128 * 2 + 64 * 128 * 2
+    assert a >= 56 * 8 * per
+    assert la.la_prefill_workspace_bytes(la.make_shape(1, 8, 96, 128, 256), 100) == 0
+    assert la.la_prefill_workspace_bytes(la.make_shape(1, 8, 128, 128, 256, chunk=32), 100) == 0
+    assert la.la_prefill_workspace_bytes(la.make_shape(1, 8, 128, 128, 0), 100) == 0
+
+
+FAKE = 1 << 20          # 16-byte aligned dummy device address (never dereferenced)
+
+
+def _resume_status(shape, cu, starts, ws_bytes=1 << 40):
+    lib = la.library()
+    cu = np.asarray(cu, np.int32)
+    starts = np.asarray(starts, np.int64)
+    P = lambda a: a.ctypes.data_as(la.ctypes.c_void_p)
+    return lib.la_prefill_resume(la.ctypes.byref(shape), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, P(cu),
+                                 FAKE, P(starts), FAKE, FAKE, FAKE, None, None, None,
+                                 FAKE, ws_bytes, None)
+
+
+def test_resume_rejects_empty_suffix_before_launch():
+    sh = la.make_shape(2, 8, 128, 128, 256)
+    assert _resume_status(sh, [0, 256, 256], [3328, 3584]) == la.LA_ERR_EMPTY_SUFFIX
+    assert "empty suffix" in la.last_error_message()
+
+
+def test_resume_rejects_misaligned_state_before_launch():
+    sh = la.make_shape(1, 8, 128, 128, 256)
+    assert _resume_status(sh, [0, 256], [3327]) == la.LA_ERR_MISALIGNED_STATE
+
+
+def test_resume_rejects_bad_tables_and_shapes():
+    sh = la.make_shape(1, 8, 128, 128, 256)
+    assert _resume_status(sh, [5, 256], [0]) == la.LA_ERR_INVALID_ARG          # cu[0] != 0
+    assert _resume_status(la.make_shape(2, 8, 128, 128, 256), [0, 300, 200], [0, 0]) == la.LA_ERR_INVALID_ARG
+    assert _resume_status(sh, [0, 256], [-256]) == la.LA_ERR_INVALID_ARG
+    assert _resume_status(la.make_shape(1, 8, 96, 128, 256), [0, 256], [0]) == la.LA_ERR_UNSUPPORTED
+    assert _resume_status(la.make_shape(1, 8, 128, 128, 256, chunk=32), [0, 256], [0]) == la.LA_ERR_UNSUPPORTED
+    assert _resume_status(la.make_shape(1, 8, 128, 128, 256, io_dtype=7), [0, 256], [0]) == la.LA_ERR_INVALID_ARG
+    assert _resume_status(la.make_shape(1, 8, 128, 128, 256, variant=3), [0, 256], [0]) == la.LA_ERR_INVALID_ARG
+    assert _resume_status(la.make_shape(0, 8, 128, 128, 256), [0], []) == la.LA_ERR_INVALID_ARG
+
+
+def test_short_workspace_is_rejected_before_launch():
+    sh = la.make_shape(1, 8, 128, 128, 256)
+    need = la.la_prefill_workspace_bytes(sh, 256)
+    assert _resume_status(sh, [0, 256], [3328], ws_bytes=need - 1) == la.LA_ERR_WORKSPACE
+
+
+def test_paged_validation_before_launch():
+    lib = la.library()
+    assert lib.la_state_save_paged(FAKE, 4, 6, FAKE, 8, FAKE, None, None) == la.LA_ERR_INVALID_ARG
+    assert lib.la_state_restore_paged(FAKE, 8, FAKE, FAKE, 4, 0, None, None) == la.LA_ERR_INVALID_ARG
+    assert lib.la_state_save_paged(FAKE + 4, 4, 8, FAKE, 8, FAKE, None, None) == la.LA_ERR_INVALID_ARG
+    assert lib.la_state_save_paged(FAKE, 0, 8, FAKE, 8, FAKE, None, None) == la.LA_OK   # nothing to do
+
+
+def test_status_strings():
+    assert la.status_string(la.LA_ERR_EMPTY_SUFFIX) == "LA_ERR_EMPTY_SUFFIX"
+    assert la.status_string(99) == "LA_ERR_UNKNOWN"
