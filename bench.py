@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Benchmark of the strict-prefix linear-attention prefill on one MI355X.
+
+One step is one pass of the whole path over the one-TP-rank workload
+(8 heads, dk = dv = 128, T = 3,584 bf16 tokens, fp32 state, chunk 64,
+checkpoint interval C = 256):
+
+  1. strict-prefix boundary on the host: B = 3,328 for N = 3,584;
+  2. cold prefill of all 3,584 tokens, emitting 14 fp32 checkpoints;
+  3. paged save of the 14 x 8 checkpoint pages into a pool through a
+     random-permutation page table;
+  4. paged restore of the 8 pages of the checkpoint at B;
+  5. resume over the 256-token suffix [B, N) from the restored state.
+
+Inputs are resident in HBM before timing starts.  The JSON line reports
+whole-step prefill tokens/s (3,584 + 256 tokens per step), the dominant
+kernel's roofline (per-kernel durations from HIP events recorded inside the
+library on the launch stream), paged save/restore bandwidth on the full
+4,096-page pool, and the fp64 CPU oracle's rate on the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0            # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0         # MI355X dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3          # MI355X dense fp32 MFMA
+CHUNK = 64
+
+
+class HipEvents:
+    """Raw hipEvent_t handles from the HIP runtime torch uses."""
+
+    def __init__(self, n):
+        import torch  # noqa: F401  (binds the same libamdhip64 torch loaded)
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.ev = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            assert self.hip.hipEventCreate(ctypes.byref(e)) == 0
+            self.ev.append(e.value)
+
+    def record(self, i, stream):
+        assert self.hip.hipEventRecord(self.ev[i], stream) == 0
+
+    def ms(self, a, b):
+        assert self.hip.hipEventSynchronize(self.ev[b]) == 0
+        out = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(out), self.ev[a], self.ev[b]) == 0
+        return float(out.value)
+
+
+def flops_per_token_head(dk, dv, L=CHUNK):
+    """Algorithmic flops per (token, head), triangular products counted once.
+
+    prep:  K K^T (L dk), W = X (..K) (L dk), U~ = X (..V) (L dv), inverse (L^2 / 3)
+    scan:  W S (2 dk dv), K~^T U (2 dk dv)
+    out:   Q S (2 dk dv), Q K^T (L dk), P U (L dv)
+    """
+    return {"prep": 2 * L * dk + L * dv + L * L / 3,
+            "scan": 4 * dk * dv,
+            "out": 2 * dk * dv + L * dk + L * dv}
+
+
+def cpu_baseline(w, B, seconds):
+    """The fp64 oracle on the same workload (cold prefill + resume), repeated
+    until about ``seconds`` of CPU time; threads over heads."""
+    import oracle
+    x, C, N = w.inputs, w.interval, w.inputs.total_tokens
+    threads = min(x.n_heads, len(os.sched_getaffinity(0)))
+    t0 = time.perf_counter()
+    reps = 0
+    used = threads
+    while True:
+        _, _, ck, used = oracle.gdr_prefill_seq(x.q, x.k, x.v, x.g, x.beta, interval=C,
+                                                n_threads=threads, return_threads=True)
+        xs = x.tokens(B, N)
+        oracle.gdr_prefill_seq(xs.q, xs.k, xs.v, xs.g, xs.beta, start=B, interval=C,
+                               state_in=ck[B // C - 1], n_threads=threads)
+        reps += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    tokens = reps * (N + (N - B))
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": used, "kind": "oracle",
+            "sample": f"{reps} x (cold prefill {N} tok + resume {N - B} tok) x {x.n_heads} heads, "
+                      f"fp64 token loop, {dt:.1f} s wall"}
+
+
+def bench_pool(la, torch, stream_ptr, events, n_pages=4096, page_elems=128 * 128, reps=20):
+    """Full-pool scatter and gather under a random permutation (2 x 256 MiB)."""
+    rng = np.random.default_rng(7)
+    perm = torch.from_numpy(rng.permutation(n_pages).astype(np.int32)).cuda()
+    states = torch.randn((n_pages, page_elems), device="cuda")
+    pool = torch.empty((n_pages, page_elems), device="cuda")
+    back = torch.empty_like(states)
+    for _ in range(3):
+        la.la_state_save_paged(states, pool, perm)
+        la.la_state_restore_paged(pool, perm, back)
+    torch.cuda.synchronize()
+    assert torch.equal(back, states)
+    ms_save = ms_restore = 0.0
+    for _ in range(reps):
+        events.record(4, stream_ptr)
+        la.la_state_save_paged(states, pool, perm)
+        events.record(5, stream_ptr)
+        la.la_state_restore_paged(pool, perm, back)
+        events.record(6, stream_ptr)
+        ms_save += events.ms(4, 5)
+        ms_restore += events.ms(5, 6)
+    nbytes = 2.0 * n_pages * page_elems * 4           # read + write
+    save = nbytes / (ms_save / reps * 1e-3) / 1e9
+    restore = nbytes / (ms_restore / reps * 1e-3) / 1e9
+    return {"pages": n_pages, "page_bytes": page_elems * 4, "bytes_per_call": nbytes,
+            "save_GBps": round(save, 1), "restore_GBps": round(restore, 1),
+            "save_frac_hbm": round(save / HBM_PEAK_GBPS, 4),
+            "restore_frac_hbm": round(restore / HBM_PEAK_GBPS, 4),
+            "save_us": round(ms_save / reps * 1e3, 2), "restore_us": round(ms_restore / reps * 1e3, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-pool", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this path holds one tensor-parallel rank's heads and "
+              "needs no collectives; run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_15030_amd import api
+    from paper_2609_15030_amd import linattn as la
+    from paper_2609_15030_amd import workloads as wl
+
+    torch.cuda.set_device(0)
+    w = wl.tp_rank_3584()
+    x, C = w.inputs, w.interval
+    N, H, dk, dv = x.total_tokens, x.n_heads, x.dk, x.dv
+    B = la.strict_prefix_boundary(N, C, w.available[0])
+    xd = api.to_device(x)
+    xs = api.to_device(x.tokens(B, N))
+    cold = api.Prefill(xd, C)
+    resume = api.Prefill(xs, C, starts=[B])
+    n_ck = cold.n_ckpt_rows
+    rng = np.random.default_rng(11)
+    pool = torch.empty((n_ck * H, dk * dv), dtype=torch.float32, device="cuda")
+    save_ids = torch.from_numpy(rng.permutation(n_ck * H).astype(np.int32)).cuda()
+    j = B // C - 1
+    restore_ids = save_ids[j * H:(j + 1) * H].contiguous()
+    restored = torch.empty((1, H, dk, dv), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    ev = HipEvents(10)
+    stage_ev = [ev.ev[0], ev.ev[1], ev.ev[2], ev.ev[3]]
+
+    def step(trace):
+        b = la.strict_prefix_boundary(N, C, w.available[0])
+        assert b == B
+        if trace:
+            la.la_trace_set_events(stage_ev)
+        cold.run()
+        if trace:
+            la.la_trace_set_events([])
+        la.la_state_save_paged(cold.ckpt, pool, save_ids)
+        la.la_state_restore_paged(pool, restore_ids, restored)
+        resume.run(restored)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    # parity guard on the benchmarked buffers: resume equals the cold run's tail
+    assert torch.equal(resume.o, cold.o[B:]) and torch.equal(resume.final, cold.final)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev.record(8, sp)
+    for _ in range(args.steps):
+        step(False)
+    ev.record(9, sp)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev.ms(8, 9)
+    ms_per_step = wall * 1e3 / args.steps
+    tokens_per_step = N + (N - B)
+
+    # per-kernel durations of the cold prefill, from events inside the library
+    stage = {"prep": 0.0, "scan": 0.0, "out": 0.0}
+    n_trace = max(10, args.steps // 2)
+    for _ in range(n_trace):
+        step(True)
+        stage["prep"] += ev.ms(0, 1)
+        stage["scan"] += ev.ms(1, 2)
+        stage["out"] += ev.ms(2, 3)
+    stage_us = {k: v / n_trace * 1e3 for k, v in stage.items()}
+    fl = flops_per_token_head(dk, dv)
+    dom = max(stage_us, key=stage_us.get)
+    achieved = fl[dom] * N * H / (stage_us[dom] * 1e-6) / 1e12
+    prefill_us = sum(stage_us.values())
+    roofline = {"bound": "mfma", "kernel": {"prep": "gdr_prep_kernel", "scan": "gdr_scan_kernel",
+                                             "out": "gdr_out_kernel"}[dom],
+                "achieved": round(achieved, 3), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 5), "traffic": None,
+                "flops_per_launch": fl[dom] * N * H, "avg_launch_us": round(stage_us[dom], 2)}
+
+    out = {
+        "metric": "linear-attn prefill tokens/s per rank + % MFMA peak; state save/restore GB/s",
+        "value": round(tokens_per_step * args.steps / wall, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "n_seqs": 1, "heads": H, "dk": dk, "dv": dv, "T": N,
+                   "chunk": CHUNK, "ckpt_interval": C, "restore_at": B,
+                   "tokens_per_step": tokens_per_step},
+        "gpu_ms_per_step": round(gpu_ms / args.steps, 4),
+        "cold_prefill": {"us": round(prefill_us, 2), "tokens_per_s": round(N / (prefill_us * 1e-6), 1),
+                         "stage_us": {k: round(v, 2) for k, v in stage_us.items()},
+                         "alg_tflops": round(sum(fl.values()) * N * H / (prefill_us * 1e-6) / 1e12, 3)},
+        "roofline": roofline,
+    }
+    if not args.no_pool:
+        out["save_restore"] = bench_pool(la, torch, sp, ev)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, B, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

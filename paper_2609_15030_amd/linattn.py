@@ -59,6 +59,11 @@ def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with "
                           "`python -m paper_2609_15030_amd.build` (hipcc, gfx950)")
+    # The library must share one HIP runtime with torch (which owns device
+    # memory and streams).  torch ships its own libamdhip64.so.7; loading
+    # torch first makes the dynamic linker bind our dependency to that copy
+    # instead of loading a second runtime from the ROCm install.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     SH = ctypes.POINTER(LaShape)

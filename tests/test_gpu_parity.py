@@ -154,6 +154,7 @@ def test_resume_rejects_empty_suffix_and_misaligned_state():
     xd = api.to_device(x)
     st = torch.zeros((1, 1, 64, 64), device="cuda")
     p = api.Prefill(xd, 64, starts=[64])
+    p.o.fill_(7.0)
     o_before = p.o.clone()
     # misaligned: B = 32 is not a multiple of C = 64
     p.starts[:] = 32
