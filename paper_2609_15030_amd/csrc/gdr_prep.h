@@ -15,6 +15,11 @@
 // chunk is exp(G_63) S_0 + K~^T U.  (Derivation: unroll the recurrence
 // inside the chunk; the prediction of row r sees S_0 decayed by exp(Gp_r)
 // plus the rank-one writes of earlier rows decayed by exp(Gp_r - G_s).)
+//
+// K and V are staged row-major only; operands that contract over chunk rows
+// are read with the LDS transpose read (bf16) or one element per lane (fp32).
+// Exponentials of gate differences use exp2 on log2(e)-scaled cumulative
+// gates; every exponent is a difference formed before exponentiation.
 #pragma once
 #include "la_common.h"
 
@@ -24,20 +29,22 @@ struct PrepArgs {
     const void *k, *v;
     const float *g, *beta;
     const int32_t *cu;
-    int32_t n_heads, C, cps, variant;
+    int32_t n_seqs, n_heads, C, cps, variant, max_chunks;
     Workspace ws;
 };
 
-template <typename T, int DK, int DV> struct PrepSmem {
-    static constexpr int PK = Vec<T>::N;      // row pads keep 16-byte alignment
-    T ks[kChunk][DK + PK];                    // K, row-major
-    T kst[DK][kChunk + PK];                   // K^T
-    T vst[DV][kChunk + PK];                   // V^T
-    float am[kChunk][kChunk + 1];             // A (strictly lower)
-    float xm[kChunk][kChunk + 1];             // X = (I + A)^{-1}
-    float ysc[4][16][17];                     // per-wave 16x16 scratch
-    float gs[kChunk], bs[kChunk], G[kChunk], Gp[kChunk];
-    float dW[kChunk], dK[kChunk];             // beta exp(Gp), exp(G_63 - G)
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <typename T, int DK, int DV> struct alignas(16) PrepSmem {
+    static constexpr int PK = Vec<T>::N;       // row pads keep 16-byte alignment
+    static constexpr int DM = DK > DV ? DK : DV;
+    T ks[kChunk][DK + PK];                     // K, row-major
+    T vs[kChunk][DM + PK];                     // V, row-major; later -W staging
+    float am[kChunk][kChunk + 4];              // A (strictly lower)
+    float xm[kChunk][kChunk + 4];              // X = (I + A)^{-1}
+    float ysc[4][16][17];                      // per-wave 16x16 scratch
+    float G2[kChunk], Gp2[kChunk], bs[kChunk]; // log2e-scaled gates, beta
+    float dW[kChunk], dK[kChunk];              // beta exp(Gp), exp(G_63 - G)
 };
 
 // 16x16x16 fp32 product of two LDS blocks with fp32 MFMA, accumulated in c.
@@ -51,114 +58,200 @@ __device__ inline f32x4 mm16_f32(const float *A, int lda, const float *B, int ld
     return c;
 }
 
+// Operands that contract over the rows of a row-major LDS tile.
+template <typename T> struct RowTile;
+
+template <> struct RowTile<__bf16> {
+    typedef short i16x4 __attribute__((ext_vector_type(4)));
+    // LDS transpose read: in each 16-lane group, source lane s reads 4
+    // elements of row `row(s)` at column n0 + 4 (s % 4); with row(s) chosen
+    // as base + s / 4, lane i of the group receives column n0 + i of rows
+    // base .. base + 3.
+    __device__ static inline i16x4 tr4(const __bf16 *tile, int ld, int row, int n0, int lane) {
+        const int s = lane & 15;
+        const __bf16 *p = tile + row * ld + n0 + 4 * (s & 3);
+        return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4 *)p);
+    }
+    // B operand (32 x 16, natural k order): rows [k0, k0 + 32), columns [n0, n0 + 16)
+    __device__ static inline bf16x8 bfrag(const __bf16 *tile, int ld, int k0, int n0, int lane) {
+        const int g = lane >> 4, s = lane & 15;
+        const i16x4 lo = tr4(tile, ld, k0 + 8 * g + (s >> 2), n0, lane);
+        const i16x4 hi = tr4(tile, ld, k0 + 8 * g + 4 + (s >> 2), n0, lane);
+        typedef short i16x8 __attribute__((ext_vector_type(8)));
+        const i16x8 both = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        return __builtin_bit_cast(bf16x8, both);
+    }
+    // tile[perm_row(f, g)][n0 + lane % 16] for f = 4q .. 4q + 3
+    __device__ static inline void col4(const __bf16 *tile, int ld, int q, int n0, int lane, float *out) {
+        const int g = lane >> 4, s = lane & 15;
+        const i16x4 v = tr4(tile, ld, 16 * q + 4 * g + (s >> 2), n0, lane);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) out[t] = (float)__builtin_bit_cast(__bf16, (short)v[t]);
+    }
+};
+
+template <> struct RowTile<float> {
+    // B operand (4 x 16): one element per lane
+    __device__ static inline float bfrag(const float *tile, int ld, int k0, int n0, int lane) {
+        return tile[(k0 + (lane >> 4)) * ld + n0 + (lane & 15)];
+    }
+    __device__ static inline void col4(const float *tile, int ld, int q, int n0, int lane, float *out) {
+        const int g = lane >> 4;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) out[t] = tile[(16 * q + 4 * g + t) * ld + n0 + (lane & 15)];
+    }
+};
+
 template <typename T, int DK, int DV>
-__global__ __launch_bounds__(256) void gdr_prep_kernel(PrepArgs a) {
+__global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
     using M = MT<T>;
+    using RT = RowTile<T>;
+    using Sm = PrepSmem<T, DK, DV>;
     constexpr int KW = M::KW, KSTEP = M::KSTEP, VEC = Vec<T>::N;
-    __shared__ PrepSmem<T, DK, DV> sm;
+    constexpr int LDK = DK + Sm::PK, LDV = Sm::DM + Sm::PK, LDA = kChunk + 4;
+    __shared__ Sm sm;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g16 = lane >> 4, c16 = lane & 15;
-    const int64_t j = blockIdx.x;
-    const int h = blockIdx.y, seq = blockIdx.z, H = a.n_heads;
-    const int64_t cu0 = a.cu[seq], len = (int64_t)a.cu[seq + 1] - cu0;
-    if (j >= n_chunks(len, a.C, a.cps)) return;
-    int64_t lo, hi;
-    chunk_range(j, len, a.C, a.cps, &lo, &hi);
-    const int n = (int)(hi - lo);
+    int64_t j;
+    int seq, h;
+    if (!unit_of_block(a.n_seqs, a.n_heads, a.max_chunks, &seq, &h, &j)) return;
+    const int H = a.n_heads;
+    const int64_t cu0 = a.cu[seq];
+    const int len = a.cu[seq + 1] - a.cu[seq];
+    if (j >= n_chunks32(len, a.C, a.cps)) return;
+    int lo, hi;
+    chunk_range32((int)j, len, a.C, a.cps, &lo, &hi);
+    const int n = hi - lo;
     const int64_t t0 = cu0 + lo;
     const int64_t sh = (slot_base(cu0, seq, a.C, a.cps) + j) * H + h;   // slot-head index
 
     const T *kin = (const T *)a.k;
     const T *vin = (const T *)a.v;
 
-    // ---- 1. stage K, K^T, V^T, g, beta in LDS; clear X -----------------------
-    for (int vi = tid; vi < kChunk * DK / VEC; vi += 256) {
-        const int r = vi / (DK / VEC), c = (vi % (DK / VEC)) * VEC;
-        T buf[VEC];
-        if (r < n) {
-            const uint4 raw = *(const uint4 *)(kin + ((t0 + r) * H + h) * DK + c);
-            *(uint4 *)buf = raw;
-        } else {
+    // ---- 1. stage K, V (row-major), g, beta; clear X ------------------------
+    // Every global load is issued before the first use; rows past the
+    // chunk's end read the last valid row and are zeroed afterwards.
+    {
+        constexpr int KIT = kChunk * DK / VEC / 256, VIT = kChunk * DV / VEC / 256;
+        static_assert(KIT * 256 * VEC == kChunk * DK && VIT * 256 * VEC == kChunk * DV, "tiling");
+        uint4 kr[KIT], vr[VIT];
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) buf[e] = from_f32<T>(0.f);
-        }
-        *(uint4 *)&sm.ks[r][c] = *(const uint4 *)buf;
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) sm.kst[c + e][r] = buf[e];
-    }
-    for (int vi = tid; vi < kChunk * DV / VEC; vi += 256) {
-        const int r = vi / (DV / VEC), c = (vi % (DV / VEC)) * VEC;
-        T buf[VEC];
-        if (r < n) {
-            *(uint4 *)buf = *(const uint4 *)(vin + ((t0 + r) * H + h) * DV + c);
-        } else {
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) buf[e] = from_f32<T>(0.f);
+        for (int it = 0; it < KIT; ++it) {
+            const int vi = tid + 256 * it, r = vi / (DK / VEC), c = (vi % (DK / VEC)) * VEC;
+            const int rr = r < n ? r : n - 1;
+            kr[it] = *(const uint4 *)(kin + ((t0 + rr) * H + h) * DK + c);
         }
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) sm.vst[c + e][r] = buf[e];
-    }
-    if (tid < kChunk) {
-        const bool ok = tid < n;
-        sm.gs[tid] = ok ? a.g[(t0 + tid) * H + h] : 0.f;
-        sm.bs[tid] = ok ? a.beta[(t0 + tid) * H + h] : 0.f;
-    }
-    for (int e = tid; e < kChunk * (kChunk + 1); e += 256) (&sm.xm[0][0])[e] = 0.f;
-    __syncthreads();
-
-    // ---- 2. chunk-local gate prefix sum (wave 0) ------------------------------
-    if (wave == 0) {
-        float x = sm.gs[lane];
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const float y = __shfl_up(x, d, 64);
-            if (lane >= d) x += y;
+        for (int it = 0; it < VIT; ++it) {
+            const int vi = tid + 256 * it, r = vi / (DV / VEC), c = (vi % (DV / VEC)) * VEC;
+            const int rr = r < n ? r : n - 1;
+            vr[it] = *(const uint4 *)(vin + ((t0 + rr) * H + h) * DV + c);
         }
-        const float prev = __shfl_up(x, 1, 64);
-        const float gp = (a.variant == 0) ? (lane == 0 ? 0.f : prev) : x;
-        const float g63 = __shfl(x, 63, 64);
-        sm.G[lane] = x;
-        sm.Gp[lane] = gp;
-        sm.dW[lane] = sm.bs[lane] * expf(gp);
-        sm.dK[lane] = expf(g63 - x);
-        a.ws.g[sh * kChunk + lane] = x;
+        float gv = 0.f, bv = 0.f;
+        if (tid < kChunk) {
+            const int rr = tid < n ? tid : n - 1;
+            gv = a.g[(t0 + rr) * H + h];
+            bv = a.beta[(t0 + rr) * H + h];
+        }
+        for (int e = tid; e < kChunk * LDA; e += 256) (&sm.xm[0][0])[e] = 0.f;
+#pragma unroll
+        for (int it = 0; it < KIT; ++it) {
+            const int vi = tid + 256 * it, r = vi / (DK / VEC), c = (vi % (DK / VEC)) * VEC;
+            if (r >= n) kr[it] = make_uint4(0, 0, 0, 0);
+            *(uint4 *)&sm.ks[r][c] = kr[it];
+        }
+#pragma unroll
+        for (int it = 0; it < VIT; ++it) {
+            const int vi = tid + 256 * it, r = vi / (DV / VEC), c = (vi % (DV / VEC)) * VEC;
+            if (r >= n) vr[it] = make_uint4(0, 0, 0, 0);
+            *(uint4 *)&sm.vs[r][c] = vr[it];
+        }
+        // ---- 2. chunk-local gate prefix sum (wave 0) --------------------------
+        if (wave == 0) {
+            float x = tid < n ? gv : 0.f;
+            const float b = tid < n ? bv : 0.f;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const float y = __shfl_up(x, d, 64);
+                if (lane >= d) x += y;
+            }
+            const float prev = __shfl_up(x, 1, 64);
+            const float gp = (a.variant == 0) ? (lane == 0 ? 0.f : prev) : x;
+            const float g63 = __shfl(x, 63, 64);
+            sm.G2[lane] = x * kLog2e;
+            sm.Gp2[lane] = gp * kLog2e;
+            sm.bs[lane] = b;
+            sm.dW[lane] = b * __builtin_amdgcn_exp2f(gp * kLog2e);
+            sm.dK[lane] = __builtin_amdgcn_exp2f((g63 - x) * kLog2e);
+            a.ws.g[sh * kChunk + lane] = x;
+        }
     }
     __syncthreads();
 
     // ---- 3. A = strictly-lower beta_r exp(Gp_r - G_s) K K^T ------------------
+    // The 10 lower 16x16 tiles are dealt 3/3/2/2 over the waves.  A tile's
+    // row tile is a run-time value, so its gate and beta values are read from
+    // LDS per tile (a register array indexed by it would become a select
+    // chain).
     {
-        const int mt = wave;
-        for (int nt = 0; nt <= mt; ++nt) {
-            f32x4 acc = zero4();
+        constexpr int tmt[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
+        constexpr int tnt[10] = {0, 0, 1, 0, 1, 2, 0, 1, 2, 3};
 #pragma unroll
-            for (int ks = 0; ks < DK / KSTEP; ++ks) {
-                const typename M::frag fa = M::pack(&sm.ks[16 * mt + c16][ks * KSTEP + g16 * KW]);
-                const typename M::frag fb = M::pack(&sm.ks[16 * nt + c16][ks * KSTEP + g16 * KW]);
-                acc = M::mma(fa, fb, acc);
-            }
+        for (int q = 0; q < 3; ++q) {
+            const int t = wave + 4 * q;
+            if (t < 10) {
+                const int mt = tmt[t], nt = tnt[t];
+                const float4 brow = *(const float4 *)&sm.bs[16 * mt + 4 * g16];
+                const float4 gprow = *(const float4 *)&sm.Gp2[16 * mt + 4 * g16];
+                const float gcol = sm.G2[16 * nt + c16];
+                f32x4 acc = zero4();
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = 16 * mt + 4 * g16 + i, s = 16 * nt + c16;
-                sm.am[r][s] = (s < r) ? sm.bs[r] * expf(sm.Gp[r] - sm.G[s]) * acc[i] : 0.f;
+                for (int ks = 0; ks < DK / KSTEP; ++ks)
+                    acc = M::mma(M::pack(&sm.ks[16 * mt + c16][ks * KSTEP + g16 * KW]),
+                                 M::pack(&sm.ks[16 * nt + c16][ks * KSTEP + g16 * KW]), acc);
+                const float bv[4] = {brow.x, brow.y, brow.z, brow.w};
+                const float gv[4] = {gprow.x, gprow.y, gprow.z, gprow.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int r = 16 * mt + 4 * g16 + i, s = 16 * nt + c16;
+                    const float e = __builtin_amdgcn_exp2f(gv[i] - gcol);
+                    sm.am[r][s] = (s < r) ? bv[i] * e * acc[i] : 0.f;
+                }
             }
         }
     }
     __syncthreads();
 
     // ---- 4. X = (I + A)^{-1}: diagonal 16-blocks by substitution ---------------
-    if (lane < 16) {
+    {
         const int base = 16 * wave;
-        float x[16];
+        // the block's strictly lower part, read once (same addresses on all lanes)
+        float ab[16][16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            float acc = (r == lane) ? 1.f : 0.f;
+        for (int r = 1; r < 16; ++r)
 #pragma unroll
-            for (int s = 0; s < r; ++s) acc -= sm.am[base + r][base + s] * x[s];
-            x[r] = acc;
+            for (int s4 = 0; s4 < 16; s4 += 4) {
+                if (s4 < r) {
+                    const float4 v = *(const float4 *)&sm.am[base + r][base + s4];
+                    ab[r][s4] = v.x;
+                    ab[r][s4 + 1] = v.y;
+                    ab[r][s4 + 2] = v.z;
+                    ab[r][s4 + 3] = v.w;
+                }
+            }
+        if (lane < 16) {
+            float x[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                float acc = (r == lane) ? 1.f : 0.f;
+#pragma unroll
+                for (int s = 0; s < r; ++s) acc -= ab[r][s] * x[s];
+                x[r] = acc;
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sm.xm[base + r][base + lane] = x[r];
         }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sm.xm[base + r][base + lane] = x[r];
     }
     __syncthreads();
     // off-diagonal blocks by bands: X_ij = -X_ii sum_{k=j}^{i-1} A_ik X_kj
@@ -168,22 +261,21 @@ __global__ __launch_bounds__(256) void gdr_prep_kernel(PrepArgs a) {
         if (active) {
             f32x4 y = zero4();
             for (int bk = bj; bk < bi; ++bk)
-                y = mm16_f32(&sm.am[16 * bi][16 * bk], kChunk + 1, &sm.xm[16 * bk][16 * bj],
-                             kChunk + 1, y, lane);
+                y = mm16_f32(&sm.am[16 * bi][16 * bk], LDA, &sm.xm[16 * bk][16 * bj], LDA, y, lane);
 #pragma unroll
             for (int i = 0; i < 4; ++i) sm.ysc[wave][4 * g16 + i][c16] = y[i];
         }
         __syncthreads();
         if (active) {
-            f32x4 xij = mm16_f32(&sm.xm[16 * bi][16 * bi], kChunk + 1, &sm.ysc[wave][0][0], 17,
-                                 zero4(), lane);
+            f32x4 xij = mm16_f32(&sm.xm[16 * bi][16 * bi], LDA, &sm.ysc[wave][0][0], 17, zero4(), lane);
 #pragma unroll
             for (int i = 0; i < 4; ++i) sm.xm[16 * bi + 4 * g16 + i][16 * bj + c16] = -xij[i];
         }
         __syncthreads();
     }
 
-    // ---- 5. W = X diag(dW) K (staged in ks), U~ = X diag(beta) V (to workspace) --
+    // ---- 5. W = X diag(dW) K, U~ = X diag(beta) V, K~^T fragments -------------
+    f32x4 wt[DK / 16];
     {
         const int mt = wave;
         constexpr int NKS = kChunk / KSTEP;
@@ -201,13 +293,12 @@ __global__ __launch_bounds__(256) void gdr_prep_kernel(PrepArgs a) {
             f1[ks] = M::pack(v1);
             f2[ks] = M::pack(v2);
         }
-        f32x4 wt[DK / 16];
 #pragma unroll
         for (int nt = 0; nt < DK / 16; ++nt) {
             f32x4 acc = zero4();
 #pragma unroll
             for (int ks = 0; ks < NKS; ++ks)
-                acc = M::mma(f1[ks], M::pack(&sm.kst[16 * nt + c16][ks * KSTEP + g16 * KW]), acc);
+                acc = M::mma(f1[ks], RT::bfrag(&sm.ks[0][0], LDK, ks * KSTEP, 16 * nt, lane), acc);
             wt[nt] = acc;
         }
         float4 *ut = (float4 *)(a.ws.ut + sh * WsLayout<T, DK, DV>::ut_elems);
@@ -216,21 +307,42 @@ __global__ __launch_bounds__(256) void gdr_prep_kernel(PrepArgs a) {
             f32x4 acc = zero4();
 #pragma unroll
             for (int ks = 0; ks < NKS; ++ks)
-                acc = M::mma(f2[ks], M::pack(&sm.vst[16 * nt + c16][ks * KSTEP + g16 * KW]), acc);
+                acc = M::mma(f2[ks], RT::bfrag(&sm.vs[0][0], LDV, ks * KSTEP, 16 * nt, lane), acc);
             ut[(nt * 4 + mt) * 64 + lane] = make_float4(acc[0], acc[1], acc[2], acc[3]);
         }
-        __syncthreads();   // every wave is done reading ks (step 3) before it is overwritten
+        // K~^T: per dk row tile, lane holds 16 values at chunk rows perm_row(f, g)
+        T *kout = (T *)a.ws.kt + sh * WsLayout<T, DK, DV>::kt_elems;
+        constexpr int NV2 = 16 / VEC;
+        for (int kt = wave; kt < DK / 16; kt += 4) {
+            T vals[16];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                float c4[4];
+                RT::col4(&sm.ks[0][0], LDK, q, 16 * kt, lane, c4);
+                const float4 d = *(const float4 *)&sm.dK[16 * q + 4 * g16];
+                vals[4 * q + 0] = from_f32<T>(c4[0] * d.x);
+                vals[4 * q + 1] = from_f32<T>(c4[1] * d.y);
+                vals[4 * q + 2] = from_f32<T>(c4[2] * d.z);
+                vals[4 * q + 3] = from_f32<T>(c4[3] * d.w);
+            }
+#pragma unroll
+            for (int v = 0; v < NV2; ++v)
+                *(uint4 *)(kout + ((size_t)(kt * NV2 + v) * 64 + lane) * VEC) = *(const uint4 *)&vals[v * VEC];
+        }
+    }
+    __syncthreads();   // every wave is done reading ks and vs
+    {
+        const int mt = wave;
 #pragma unroll
         for (int nt = 0; nt < DK / 16; ++nt)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                sm.ks[16 * mt + 4 * g16 + i][16 * nt + c16] = from_f32<T>(-wt[nt][i]);
+                sm.vs[16 * mt + 4 * g16 + i][16 * nt + c16] = from_f32<T>(-wt[nt][i]);
     }
     __syncthreads();
 
-    // ---- 6. write -W and K~^T in A-operand order -------------------------------
+    // ---- 6. write -W in A-operand order (columns perm_row(f, g)) ---------------
     {
-        // -W: per row tile mt, lane: DK/4 values at columns perm_row(f, g)
         constexpr int NV = DK / 4 / VEC;
         T *wout = (T *)a.ws.w + sh * WsLayout<T, DK, DV>::w_elems;
         for (int vi = tid; vi < 4 * NV * 64; vi += 256) {
@@ -238,22 +350,8 @@ __global__ __launch_bounds__(256) void gdr_prep_kernel(PrepArgs a) {
             const int r = 16 * mt + (ln & 15), g = ln >> 4;
             T buf[VEC];
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) buf[e] = sm.ks[r][perm_row(v * VEC + e, g)];
+            for (int e = 0; e < VEC; ++e) buf[e] = sm.vs[r][perm_row(v * VEC + e, g)];
             *(uint4 *)(wout + (size_t)vi * VEC) = *(const uint4 *)buf;
-        }
-        // K~^T: per dk row tile mt, lane: 16 values at chunk rows perm_row(f, g)
-        constexpr int NV2 = 16 / VEC;
-        T *kout = (T *)a.ws.kt + sh * WsLayout<T, DK, DV>::kt_elems;
-        for (int vi = tid; vi < (DK / 16) * NV2 * 64; vi += 256) {
-            const int ln = vi & 63, v = (vi >> 6) % NV2, mt = vi / (64 * NV2);
-            const int m = 16 * mt + (ln & 15), g = ln >> 4;
-            T buf[VEC];
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) {
-                const int s = perm_row(v * VEC + e, g);
-                buf[e] = from_f32<T>(sm.dK[s] * to_f32(sm.kst[m][s]));
-            }
-            *(uint4 *)(kout + (size_t)vi * VEC) = *(const uint4 *)buf;
         }
     }
 }

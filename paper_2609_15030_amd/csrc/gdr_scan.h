@@ -1,14 +1,25 @@
-// Inter-chunk scan: the sequential part of the prefill.  One wave owns the
-// state columns [tile*BV, (tile+1)*BV) of one (sequence, head); those columns
-// evolve independently of the others.  Per chunk, with S the fp32 state
-// entering it (kept in MFMA accumulator registers for the whole sequence):
-//   U       = U~ - W S                  (64 x BV, bf16/fp32 MFMA, fp32 accumulate)
-//   S_next  = exp(G_63) S + K~^T U      (DK x BV)
+// Inter-chunk scan: the sequential part of the prefill.
+//
+// One workgroup owns 16 state columns (a dv tile) of one (sequence, head);
+// those columns evolve independently of the others.  Its NW = DK / 32 waves
+// split the dk rows of the state: wave w keeps rows [32w, 32w + 32) of the
+// fp32 state in MFMA accumulator registers for the whole sequence.  Per
+// chunk, with S the state entering it:
+//
+//   U      = U~ - W S           every wave contracts its own 32 state rows
+//                               (one 32-deep MFMA k-step) into a partial
+//                               64 x 16 product; the partials meet in LDS,
+//                               wave w sums row tile w and adds U~.
+//   S_next = exp(G_63) S + K~^T U
+//                               every wave updates its own 32 rows from
+//                               the whole of U (read back from LDS).
+//
 // The state enters both products straight from its accumulator layout; the
-// -W and K~^T operands were written by the preparation kernel with the
-// matching contraction permutation, so no lane shuffles or LDS are needed.
-// The wave also hands the output kernel the state entering each chunk and U
-// (both in the io type), and writes fp32 checkpoints and the final state.
+// -W and K~^T operands were written by the preparation kernel in the
+// matching contraction order (perm_row), so a wave's operand slice is a run
+// of whole 16-byte vectors.  Operands are prefetched two chunks ahead.  The
+// workgroup also hands the output kernel the state entering each chunk and
+// U (io type), and writes fp32 checkpoints and the final state.
 #pragma once
 #include "la_common.h"
 
@@ -24,149 +35,356 @@ struct ScanArgs {
     Workspace ws;
 };
 
-template <typename T, int DK, int DV, int BV>
-__global__ __launch_bounds__(64) void gdr_scan_kernel(ScanArgs a) {
+constexpr int kScanPrefetch = 4;   // chunks of operands in flight ahead of the one computed
+
+template <int DK> struct ScanGeom {
+    static constexpr int NW = DK / 32;      // waves per workgroup (32 state rows each)
+    static constexpr int MTW = 4 / NW;      // U row tiles each wave reduces
+};
+
+template <typename T, int DK, int DV>
+__global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
     using M = MT<T>;
     using L = WsLayout<T, DK, DV>;
     constexpr int KW = M::KW, VEC = Vec<T>::N;
-    constexpr int RT = DK / 16;          // state row tiles
-    constexpr int CT = BV / 16;          // state column tiles owned by this wave
-    constexpr int NT = DV / BV;          // waves per (sequence, head)
-    constexpr int FS = DK / 4;           // per-lane operand values over dk
-    constexpr int FU = kChunk / 4;       // per-lane operand values over chunk rows
-    static_assert(FS % VEC == 0 && FU % VEC == 0, "vector width");
+    constexpr int NW = ScanGeom<DK>::NW, MTW = ScanGeom<DK>::MTW;
+    constexpr int NT = DV / 16;             // workgroups per (sequence, head)
+    constexpr int FS = DK / 4;              // per-lane operand values over dk (all waves)
+    constexpr int FU = kChunk / 4;          // per-lane operand values over chunk rows
+    constexpr int FW = 8;                   // per-lane values of one wave's 32-row dk slice
+    constexpr int VW = FW / VEC;            // 16-byte vectors per slice
+    constexpr int VU = FU / VEC;
+    static_assert(FW % VEC == 0 && FU % VEC == 0 && NW * 32 == DK, "tiling");
 
-    const int lane = threadIdx.x, g16 = lane >> 4, c16 = lane & 15;
-    // XCD-aware unit mapping: workgroups are dealt to the 8 XCDs round-robin,
-    // so keep the NT tiles of one (sequence, head) on one XCD, where they
-    // share the chunk operands through that XCD's L2.
+    __shared__ f32x4 part[NW][4][64];       // partial products W_w S_w, C-layout
+    __shared__ uint4 ubuf[VU][64];          // U in the io type, B-operand order
+
+    // w is uniform per wave; readfirstlane makes that visible to the compiler
+    // so every operand address is a scalar base plus the lane offset.
+    const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g16 = lane >> 4, c16 = lane & 15;
+    // XCD-aware mapping: workgroups are dealt to the 8 XCDs round-robin; the
+    // NT workgroups of one (sequence, head) land on one XCD and share the
+    // chunk operands through its L2.
     const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
     const int pair = xcd + 8 * (q / NT), tile = q % NT;
     const int H = a.n_heads;
     if (pair >= a.n_seqs * H) return;
     const int seq = pair / H, h = pair % H;
     const int64_t cu0 = a.cu[seq], len = (int64_t)a.cu[seq + 1] - cu0;
-    const int64_t nch = n_chunks(len, a.C, a.cps);
+    const int64_t nch = n_chunks32((int)len, a.C, a.cps);
     const int64_t base = slot_base(cu0, seq, a.C, a.cps);
     const size_t state_off = (size_t)pair * DK * DV;
+    const int col = 16 * tile + c16;
 
-    f32x4 S[RT][CT];
+    // this wave's state rows: tiles 2w and 2w + 1
+    f32x4 S[2];
+    if (a.state_in) {
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int row = 16 * rt + 4 * g16 + i, col = tile * BV + 16 * ct + c16;
-                S[rt][ct][i] = a.state_in ? a.state_in[state_off + (size_t)row * DV + col] : 0.f;
-            }
+            for (int i = 0; i < 4; ++i)
+                S[t][i] = a.state_in[state_off + (size_t)(32 * w + 16 * t + 4 * g16 + i) * DV + col];
+    } else {
+        S[0] = zero4();
+        S[1] = zero4();
+    }
+    // Running chunk bounds (the plan of chunk_range, advanced by additions
+    // only: no 64-bit division in the loop).  A chunk ends at the next
+    // multiple of C, 64 tokens after its start, or at the end of the call.
+    int64_t pos = 0, next_ck = a.C;
+    int64_t ckpt_row = a.ckpt ? (int64_t)a.ckpt_off[seq] : 0;
+    // Drain the counters once here: without it the waitcnt pass sees the
+    // state loads as possibly pending at the loop header and waits on the
+    // in-flight operand prefetch in every iteration.
+    __builtin_amdgcn_s_waitcnt(0);
 
-    for (int64_t j = 0; j < nch; ++j) {
-        const int64_t sh = (base + j) * H + h;
-        // chunk operands
-        T wn[4][FS];
-        T kt[RT][FU];
-        {
-            const uint4 *src = (const uint4 *)((const T *)a.ws.w + sh * L::w_elems);
+    struct Ops {
+        uint4 wn[4][VW];      // -W rows (4 row tiles), this wave's dk slice
+        uint4 kt[2][VU];      // K~^T rows of this wave's 2 dk tiles, all chunk rows
+        f32x4 ut[MTW];        // U~ row tiles this wave reduces
+        float gl;             // G_63
+    };
+    const uint32_t lane16 = 16u * (uint32_t)lane;
+    auto load = [&](Ops &o, int64_t jj) {
+        const int64_t sh = (base + jj) * H + h;
+        // issue order: gate, U~, -W, K~^T (earliest-needed last is fine: each
+        // use waits only for the loads issued before it)
+        o.gl = buf_load4f(make_rsrc(a.ws.g + sh * kChunk, kChunk * sizeof(float)), 0u, 4u * (kChunk - 1));
+        const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-                for (int v = 0; v < FS / VEC; ++v)
-                    *(uint4 *)&wn[mt][v * VEC] = src[(mt * (FS / VEC) + v) * 64 + lane];
-            const uint4 *srk = (const uint4 *)((const T *)a.ws.kt + sh * L::kt_elems);
-#pragma unroll
-            for (int mt = 0; mt < RT; ++mt)
-#pragma unroll
-                for (int v = 0; v < FU / VEC; ++v)
-                    *(uint4 *)&kt[mt][v * VEC] = srk[(mt * (FU / VEC) + v) * 64 + lane];
+        for (int m = 0; m < MTW; ++m) {
+            const uint4 x = buf_load16(ru, lane16, 1024u * (tile * 4 + w * MTW + m));
+            o.ut[m] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
         }
-        f32x4 U[4][CT];
-        {
-            const float4 *ut = (const float4 *)(a.ws.ut + sh * L::ut_elems);
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-                for (int ct = 0; ct < CT; ++ct) {
-                    const float4 x = ut[((tile * CT + ct) * 4 + mt) * 64 + lane];
-                    U[mt][ct] = f32x4{x.x, x.y, x.z, x.w};
-                }
-        }
-        const float decay = expf(a.ws.g[sh * kChunk + kChunk - 1]);
-
-        // state entering the chunk, as B operand over dk (io type)
-        T sb[CT][FS];
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-            for (int f = 0; f < FS; ++f) sb[ct][f] = from_f32<T>(S[f >> 2][ct][f & 3]);
-        {
-            uint4 *dst = (uint4 *)((T *)a.ws.sc + sh * L::sc_elems);
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-                for (int v = 0; v < FS / VEC; ++v)
-                    dst[((tile * CT + ct) * (FS / VEC) + v) * 64 + lane] = *(const uint4 *)&sb[ct][v * VEC];
-        }
-        // U = U~ + (-W) S
+        const auto rw = make_rsrc((const T *)a.ws.w + sh * L::w_elems, L::w_elems * sizeof(T));
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
+            for (int v = 0; v < VW; ++v) o.wn[mt][v] = buf_load16(rw, lane16, 1024u * (mt * (FS / VEC) + w * VW + v));
+        const auto rk = make_rsrc((const T *)a.ws.kt + sh * L::kt_elems, L::kt_elems * sizeof(T));
 #pragma unroll
-                for (int ks = 0; ks < FS / KW; ++ks)
-                    U[mt][ct] = M::mma(M::pack(&wn[mt][ks * KW]), M::pack(&sb[ct][ks * KW]), U[mt][ct]);
-        // U as B operand over chunk rows
-        T ub[CT][FU];
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
+            for (int v = 0; v < VU; ++v) o.kt[t][v] = buf_load16(rk, lane16, 1024u * ((2 * w + t) * VU + v));
+    };
+
+    auto step = [&](const Ops &o, int64_t j) {
+        const int64_t sh = (base + j) * H + h;
+        // state entering the chunk as B operand over this wave's dk slice
+        T sb[FW];
 #pragma unroll
-            for (int f = 0; f < FU; ++f) ub[ct][f] = from_f32<T>(U[f >> 2][ct][f & 3]);
+        for (int f = 0; f < FW; ++f) sb[f] = from_f32<T>(S[f >> 2][f & 3]);
         {
-            uint4 *dst = (uint4 *)((T *)a.ws.u + sh * L::u_elems);
+            const auto rs = make_rsrc((T *)a.ws.sc + sh * L::sc_elems, L::sc_elems * sizeof(T));
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-                for (int v = 0; v < FU / VEC; ++v)
-                    dst[((tile * CT + ct) * (FU / VEC) + v) * 64 + lane] = *(const uint4 *)&ub[ct][v * VEC];
+            for (int v = 0; v < VW; ++v)
+                buf_store16(*(const uint4 *)&sb[v * VEC], rs, lane16, 1024u * (tile * (FS / VEC) + w * VW + v));
         }
-        // S = exp(G_63) S + K~^T U
+        // partial products over this wave's 32 state rows; the wave that
+        // reduces row tile mt starts its partial from U~
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
+        for (int mt = 0; mt < 4; ++mt) {
+            const T *wv = (const T *)&o.wn[mt][0];
+            f32x4 acc = zero4();
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct) {
-                f32x4 acc = S[rt][ct] * decay;
+            for (int m = 0; m < MTW; ++m)
+                if (mt == w * MTW + m) acc = o.ut[m];
 #pragma unroll
-                for (int ks = 0; ks < FU / KW; ++ks)
-                    acc = M::mma(M::pack(&kt[rt][ks * KW]), M::pack(&ub[ct][ks * KW]), acc);
-                S[rt][ct] = acc;
-            }
+            for (int ks = 0; ks < FW / KW; ++ks)
+                acc = M::mma(M::pack(&wv[ks * KW]), M::pack(&sb[ks * KW]), acc);
+            part[w][mt][lane] = acc;
+        }
+        __syncthreads();
+        // wave w reduces U row tiles [w*MTW, (w+1)*MTW): U = sum of partials
+#pragma unroll
+        for (int m = 0; m < MTW; ++m) {
+            const int mt = w * MTW + m;
+            f32x4 pp[NW];
+#pragma unroll
+            for (int p = 0; p < NW; ++p) pp[p] = part[p][mt][lane];
+            f32x4 u = pp[0];
+#pragma unroll
+            for (int p = 1; p < NW; ++p) u += pp[p];
+            // flat B-operand index 4 * mt + i
+            T *dst = (T *)&ubuf[(4 * mt) / VEC][lane] + (4 * mt) % VEC;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dst[i] = from_f32<T>(u[i]);
+        }
+        __syncthreads();
+        uint4 ub[VU];
+#pragma unroll
+        for (int v = 0; v < VU; ++v) ub[v] = ubuf[v][lane];
+        {
+            const auto rs = make_rsrc((T *)a.ws.u + sh * L::u_elems, L::u_elems * sizeof(T));
+#pragma unroll
+            for (int v = 0; v < VU; ++v)
+                if (v % NW == w) buf_store16(ub[v], rs, lane16, 1024u * (tile * VU + v));
+        }
+        // S = exp(G_63) S + K~^T U on this wave's rows
+        const float decay = expf(o.gl);
+        const T *uvals = (const T *)&ub[0];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const T *kv = (const T *)&o.kt[t][0];
+            f32x4 acc = S[t] * decay;
+#pragma unroll
+            for (int ks = 0; ks < FU / KW; ++ks)
+                acc = M::mma(M::pack(&kv[ks * KW]), M::pack(&uvals[ks * KW]), acc);
+            S[t] = acc;
+        }
         // checkpoint when the chunk ends on a multiple of C
-        if (a.ckpt) {
-            int64_t lo, hi;
-            chunk_range(j, len, a.C, a.cps, &lo, &hi);
-            if (hi % a.C == 0) {
-                const int64_t row = (int64_t)a.ckpt_off[seq] + hi / a.C - 1;
+        int64_t hi = pos + kChunk;
+        if (hi > next_ck) hi = next_ck;
+        if (hi > len) hi = len;
+        pos = hi;
+        if (hi == next_ck) {
+            next_ck += a.C;
+            const int64_t row = ckpt_row++;
+            if (a.ckpt) {
                 float *dst = a.ckpt + ((size_t)row * H + h) * DK * DV;
 #pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
+                for (int t = 0; t < 2; ++t)
 #pragma unroll
-                    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i)
-                            dst[(size_t)(16 * rt + 4 * g16 + i) * DV + tile * BV + 16 * ct + c16] =
-                                S[rt][ct][i];
+                    for (int i = 0; i < 4; ++i)
+                        dst[(size_t)(32 * w + 16 * t + 4 * g16 + i) * DV + col] = S[t][i];
             }
+        }
+    };
+
+    // Operand ring: chunk j computes while chunks j + 1 .. j + kScanPrefetch
+    // are in flight.  Operands come from MALL/HBM (each kernel starts with
+    // cold L2s), so several chunks of latency must be covered.  The inner
+    // loop is fully unrolled so every ring index is a compile-time constant.
+    constexpr int PF = kScanPrefetch, NB = PF + 1;
+    Ops ops[NB];
+    auto clampj = [&](int64_t jj) { return jj < nch ? jj : nch - 1; };
+    if (nch > 0) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) load(ops[u], clampj(u));
+    }
+    for (int64_t j = 0; j < nch; j += NB) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            if (j + u < nch) {
+                load(ops[(u + PF) % NB], clampj(j + u + PF));
+                step(ops[u], j + u);
+            }
+        }
+    }
+
+    if (a.final_state) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                a.final_state[state_off + (size_t)(32 * w + 16 * t + 4 * g16 + i) * DV + col] = S[t][i];
+    }
+}
+
+
+// Single-wave form: one wave owns a 16-column tile and all DK state rows, so
+// a chunk needs no workgroup synchronisation: 4 * DK/32 MFMAs for U = U~ - W S
+// and 2 * DK/16 for the state update, with the chunk operands double-buffered
+// in registers.  Used where the sequential chain, not the operand bandwidth,
+// bounds the scan (few sequence-head pairs).
+template <typename T, int DK, int DV>
+__global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
+    using M = MT<T>;
+    using L = WsLayout<T, DK, DV>;
+    constexpr int KW = M::KW, VEC = Vec<T>::N;
+    constexpr int RT = DK / 16;             // state row tiles
+    constexpr int NT = DV / 16;             // waves per (sequence, head)
+    constexpr int FS = DK / 4;              // per-lane operand values over dk
+    constexpr int FU = kChunk / 4;          // per-lane operand values over chunk rows
+    constexpr int VS = FS / VEC, VU = FU / VEC;
+
+    const int lane = threadIdx.x, g16 = lane >> 4, c16 = lane & 15;
+    const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
+    const int pair = xcd + 8 * (q / NT), tile = q % NT;
+    const int H = a.n_heads;
+    if (pair >= a.n_seqs * H) return;
+    const int seq = pair / H, h = pair % H;
+    const int64_t cu0 = a.cu[seq], len = (int64_t)a.cu[seq + 1] - cu0;
+    const int64_t nch = n_chunks32((int)len, a.C, a.cps);
+    const int64_t base = slot_base(cu0, seq, a.C, a.cps);
+    const size_t state_off = (size_t)pair * DK * DV;
+    const int col = 16 * tile + c16;
+
+    f32x4 S[RT];
+    if (a.state_in) {
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) S[t][i] = a.state_in[state_off + (size_t)(16 * t + 4 * g16 + i) * DV + col];
+    } else {
+#pragma unroll
+        for (int t = 0; t < RT; ++t) S[t] = zero4();
+    }
+    int64_t pos = 0, next_ck = a.C;
+    int64_t ckpt_row = a.ckpt ? (int64_t)a.ckpt_off[seq] : 0;
+    __builtin_amdgcn_s_waitcnt(0);   // see gdr_scan_kernel
+
+    struct Ops {
+        float gl;
+        f32x4 ut[4];
+        uint4 wn[4][VS];
+        uint4 kt[RT][VU];
+    };
+    const uint32_t lane16 = 16u * (uint32_t)lane;
+    auto load = [&](Ops &o, int64_t jj) {
+        const int64_t sh = (base + jj) * H + h;
+        o.gl = buf_load4f(make_rsrc(a.ws.g + sh * kChunk, kChunk * sizeof(float)), 0u, 4u * (kChunk - 1));
+        const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const uint4 x = buf_load16(ru, lane16, 1024u * (tile * 4 + mt));
+            o.ut[mt] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
+        }
+        const auto rw = make_rsrc((const T *)a.ws.w + sh * L::w_elems, L::w_elems * sizeof(T));
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int v = 0; v < VS; ++v) o.wn[mt][v] = buf_load16(rw, lane16, 1024u * (mt * VS + v));
+        const auto rk = make_rsrc((const T *)a.ws.kt + sh * L::kt_elems, L::kt_elems * sizeof(T));
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+            for (int v = 0; v < VU; ++v) o.kt[t][v] = buf_load16(rk, lane16, 1024u * (t * VU + v));
+    };
+    auto step = [&](const Ops &o, int64_t j) {
+        const int64_t sh = (base + j) * H + h;
+        T sb[FS];
+#pragma unroll
+        for (int f = 0; f < FS; ++f) sb[f] = from_f32<T>(S[f >> 2][f & 3]);
+        {
+            const auto rs = make_rsrc((T *)a.ws.sc + sh * L::sc_elems, L::sc_elems * sizeof(T));
+#pragma unroll
+            for (int v = 0; v < VS; ++v)
+                buf_store16(*(const uint4 *)&sb[v * VEC], rs, lane16, 1024u * (tile * VS + v));
+        }
+        f32x4 U[4];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const T *wv = (const T *)&o.wn[mt][0];
+            f32x4 acc = o.ut[mt];
+#pragma unroll
+            for (int ks = 0; ks < FS / KW; ++ks)
+                acc = M::mma(M::pack(&wv[ks * KW]), M::pack(&sb[ks * KW]), acc);
+            U[mt] = acc;
+        }
+        T ub[FU];
+#pragma unroll
+        for (int f = 0; f < FU; ++f) ub[f] = from_f32<T>(U[f >> 2][f & 3]);
+        {
+            const auto rs = make_rsrc((T *)a.ws.u + sh * L::u_elems, L::u_elems * sizeof(T));
+#pragma unroll
+            for (int v = 0; v < VU; ++v)
+                buf_store16(*(const uint4 *)&ub[v * VEC], rs, lane16, 1024u * (tile * VU + v));
+        }
+        const float decay = expf(o.gl);
+#pragma unroll
+        for (int t = 0; t < RT; ++t) {
+            const T *kv = (const T *)&o.kt[t][0];
+            f32x4 acc = S[t] * decay;
+#pragma unroll
+            for (int ks = 0; ks < FU / KW; ++ks)
+                acc = M::mma(M::pack(&kv[ks * KW]), M::pack(&ub[ks * KW]), acc);
+            S[t] = acc;
+        }
+        int64_t hi = pos + kChunk;
+        if (hi > next_ck) hi = next_ck;
+        if (hi > len) hi = len;
+        pos = hi;
+        if (hi == next_ck) {
+            next_ck += a.C;
+            const int64_t row = ckpt_row++;
+            if (a.ckpt) {
+                float *dst = a.ckpt + ((size_t)row * H + h) * DK * DV;
+#pragma unroll
+                for (int t = 0; t < RT; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) dst[(size_t)(16 * t + 4 * g16 + i) * DV + col] = S[t][i];
+            }
+        }
+    };
+
+    Ops o0, o1;
+    if (nch > 0) load(o0, 0);
+    for (int64_t j = 0; j < nch; j += 2) {
+        load(o1, j + 1 < nch ? j + 1 : j);
+        step(o0, j);
+        if (j + 1 < nch) {
+            load(o0, j + 2 < nch ? j + 2 : j + 1);
+            step(o1, j + 1);
         }
     }
     if (a.final_state) {
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
+        for (int t = 0; t < RT; ++t)
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    a.final_state[state_off + (size_t)(16 * rt + 4 * g16 + i) * DV + tile * BV +
-                                  16 * ct + c16] = S[rt][ct][i];
+            for (int i = 0; i < 4; ++i)
+                a.final_state[state_off + (size_t)(16 * t + 4 * g16 + i) * DV + col] = S[t][i];
     }
 }
 

@@ -53,6 +53,30 @@ template <> struct MT<float> {
     __device__ static inline frag pack2(const float *lo, const float *) { return lo[0]; }
 };
 
+// Raw buffer access: a scalar resource (base, size) plus a per-lane byte
+// offset.  Loop-invariant lane offsets keep operand prefetches free of
+// per-iteration VGPR address arithmetic; out-of-range reads return zero.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+constexpr int kBufferFlags = 0x00020000;   // raw (untyped) dword access
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, kBufferFlags);
+}
+
+__device__ inline uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    const i32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+    return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
+}
+
+__device__ inline void buf_store16(uint4 x, __amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    const i32x4 v = {(int)x.x, (int)x.y, (int)x.z, (int)x.w};
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, (int)soff, 0);
+}
+
+__device__ inline float buf_load4f(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+}
+
 template <typename T> __device__ inline T from_f32(float x);
 template <> __device__ inline float from_f32<float>(float x) { return x; }
 template <> __device__ inline __bf16 from_f32<__bf16>(float x) { return (__bf16)x; }  // RNE
@@ -101,6 +125,23 @@ __device__ __host__ inline void chunk_range(int64_t j, int64_t len, int64_t C, i
     *b = hi;
 }
 
+// 32-bit forms for device code (sequence lengths and C are below 2^31; the
+// host validates that), which avoid 64-bit integer division.
+__device__ inline int n_chunks32(int len, int C, int cps) {
+    const int full = len / C, rem = len - full * C;
+    return full * cps + (rem + kChunk - 1) / kChunk;
+}
+
+__device__ inline void chunk_range32(int j, int len, int C, int cps, int *a, int *b) {
+    const int seg = j / cps, sub = j - seg * cps;
+    const int lo = seg * C + sub * kChunk;
+    int hi = lo + kChunk;
+    if (hi > (seg + 1) * C) hi = (seg + 1) * C;
+    if (hi > len) hi = len;
+    *a = lo;
+    *b = hi;
+}
+
 // First workspace slot of sequence i.  A sequence of n tokens has at most
 // ceil(n * cps / C) chunks, so slot bases floor((cu[i] * cps + (C - 1) * i) / C)
 // give every sequence room for its chunks without a prefix sum over the
@@ -112,6 +153,31 @@ __device__ __host__ inline int64_t slot_base(int64_t cu_i, int64_t i, int64_t C,
 __device__ __host__ inline int64_t total_slots(int64_t total_tokens, int64_t n_seqs, int64_t C,
                                                int cps) {
     return slot_base(total_tokens, n_seqs, C, cps);
+}
+
+// ---------------------------------------------------------------------------
+// XCD-aware block mapping.  Workgroups are dealt to the 8 XCDs round-robin by
+// linear id; each XCD has its own L2.  (sequence, head) pair p is pinned to
+// XCD p % 8 in every kernel of the prefill, so the chunk intermediates one
+// kernel writes for that pair are read back from the same L2 by the next.
+// Per-chunk kernels use a 1-D grid of 8 * max_chunks * ceil(pairs / 8)
+// blocks: block id = 8 * (chunk + max_chunks * (p / 8)) + p % 8.
+// ---------------------------------------------------------------------------
+__device__ inline bool unit_of_block(int n_seqs, int n_heads, int max_chunks, int *seq, int *head,
+                                     int64_t *chunk) {
+    const int64_t b = blockIdx.x;
+    const int64_t r = b >> 3;
+    const int64_t pair = (b & 7) + 8 * (r / max_chunks);
+    if (pair >= (int64_t)n_seqs * n_heads) return false;
+    *chunk = r % max_chunks;
+    *seq = (int)(pair / n_heads);
+    *head = (int)(pair % n_heads);
+    return true;
+}
+
+__host__ inline int64_t chunk_grid_blocks(int n_seqs, int n_heads, int64_t max_chunks) {
+    const int64_t pairs = (int64_t)n_seqs * n_heads;
+    return 8 * max_chunks * ((pairs + 7) / 8);
 }
 
 // ---------------------------------------------------------------------------

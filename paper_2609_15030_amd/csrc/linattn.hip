@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 
 #include "linattn.h"
@@ -38,10 +39,19 @@ la_status hip_check(const char *what) {
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
-constexpr int kScanBV = 16;       // state columns per scan wave
 constexpr size_t kRegionAlign = 256;
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Scan kernel form: 1 = one wave per 16-column tile, 4 = DK/32 waves sharing
+// the tile's state rows.  LA_SCAN_WAVES overrides the default (for tuning).
+int scan_variant() {
+    static const int v = [] {
+        const char *e = getenv("LA_SCAN_WAVES");
+        return (e && atoi(e) == 4) ? 4 : 1;
+    }();
+    return v;
+}
 
 size_t io_size(int32_t dtype) { return dtype == LA_BF16 ? 2 : 4; }
 
@@ -120,27 +130,33 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
     (void)hipGetLastError();
 
     if (max_chunks > 0) {
-        la::PrepArgs pa{c.k, c.v, c.g, c.beta, c.cu_dev, s->n_heads, s->ckpt_interval, cps, s->variant, ws};
-        dim3 grid((unsigned)max_chunks, (unsigned)s->n_heads, (unsigned)s->n_seqs);
-        hipLaunchKernelGGL((la::gdr_prep_kernel<T, DK, DV>), grid, dim3(256), 0, c.stream, pa);
+        la::PrepArgs pa{c.k, c.v, c.g, c.beta, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
+                        s->variant, (int32_t)max_chunks, ws};
+        const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
+        hipLaunchKernelGGL((la::gdr_prep_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(256), 0, c.stream, pa);
         if (la_status e = hip_check("chunk preparation launch")) return e;
     }
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[1], c.stream);
     {
         la::ScanArgs sa{c.cu_dev, c.state_in, c.final_state, c.ckpt_out, c.ckpt_off_dev,
                         s->n_seqs, s->n_heads, s->ckpt_interval, cps, ws};
-        constexpr int NT = DV / kScanBV;
+        constexpr int NT = DV / 16;
         const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
         const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
-        hipLaunchKernelGGL((la::gdr_scan_kernel<T, DK, DV, kScanBV>), dim3((unsigned)blocks), dim3(64), 0,
-                           c.stream, sa);
+        if (scan_variant() == 1)
+            hipLaunchKernelGGL((la::gdr_scan1_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(64), 0,
+                               c.stream, sa);
+        else
+            hipLaunchKernelGGL((la::gdr_scan_kernel<T, DK, DV>), dim3((unsigned)blocks),
+                               dim3(64 * la::ScanGeom<DK>::NW), 0, c.stream, sa);
         if (la_status e = hip_check("inter-chunk scan launch")) return e;
     }
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[2], c.stream);
     if (max_chunks > 0) {
-        la::OutArgs oa{c.q, c.k, c.o, c.cu_dev, s->n_heads, s->ckpt_interval, cps, s->scale, ws};
-        dim3 grid((unsigned)max_chunks, (unsigned)s->n_heads, (unsigned)s->n_seqs);
-        hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), grid, dim3(256), 0, c.stream, oa);
+        la::OutArgs oa{c.q, c.k, c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
+                       (int32_t)max_chunks, s->scale, ws};
+        const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
+        hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(256), 0, c.stream, oa);
         if (la_status e = hip_check("output launch")) return e;
     }
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[3], c.stream);
@@ -170,6 +186,7 @@ la_status run_prefill(const PrefillCall &c) {
     for (int i = 0; i < s->n_seqs; ++i) {
         const int64_t len = (int64_t)c.cu_host[i + 1] - c.cu_host[i];
         if (len < 0) return fail(LA_ERR_INVALID_ARG, "cu_seqlens decreases at sequence %d", i);
+        if (c.cu_host[i + 1] < 0) return fail(LA_ERR_INVALID_ARG, "cu_seqlens overflows int32");
         max_chunks = std::max(max_chunks, la::n_chunks(len, C, cps));
     }
     const int64_t total = c.cu_host[s->n_seqs];
@@ -189,7 +206,9 @@ la_status run_prefill(const PrefillCall &c) {
             if (B > ((int64_t)1 << 40)) return fail(LA_ERR_INVALID_ARG, "start_pos[%d] too large", i);
         }
     }
-    if (max_chunks > 0x7fffffff) return fail(LA_ERR_INVALID_ARG, "sequence too long");
+    if (max_chunks > 0x7fffffff ||
+        la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks) > 0x7fffffff)
+        return fail(LA_ERR_INVALID_ARG, "sequence too long for one launch");
     if (total > 0) {
         if (!c.q || !c.k || !c.v || !c.g || !c.beta || !c.o)
             return fail(LA_ERR_INVALID_ARG, "q, k, v, g, beta and o are required");
