@@ -17,7 +17,7 @@
 // The state enters both products straight from its accumulator layout; the
 // -W and K~^T operands were written by the preparation kernel in the
 // matching contraction order (perm_row), so a wave's operand slice is a run
-// of whole 16-byte vectors.  Operands are prefetched two chunks ahead.  The
+// of whole 16-byte vectors.  Operands are prefetched four chunks ahead.  The
 // workgroup also hands the output kernel the state entering each chunk and
 // U (io type), and writes fp32 checkpoints and the final state.
 #pragma once
@@ -35,7 +35,64 @@ struct ScanArgs {
     Workspace ws;
 };
 
+// Chunk bounds of one sequence, advanced by additions only (the plan of
+// chunk_range without a division per chunk).  All counters are 32-bit:
+// sequence lengths and C are below 2^31, and 64-bit compares in the loop
+// would need vector temporaries that alias in-flight operand loads.
+struct ChunkCursor {
+    int pos, next_ck, len, C;
+    // Moves past the next chunk; true when that chunk ends on a multiple of C.
+    __device__ bool advance() {
+        const int hi = min(pos + kChunk, min(next_ck, len));
+        pos = hi;
+        if (hi != next_ck) return false;
+        next_ck += C;
+        return true;
+    }
+};
+
+// Writes NTILE 16-row tiles of fp32 state held in C layout (lane: column
+// voff's column, rows 4 * (lane / 16) + i of each tile) to a row-major
+// [rows, DV] block starting at dst; voff is the lane's byte offset of its
+// first row.  Buffer stores with scalar bases keep the store addresses out
+// of vector registers.
+template <int NTILE, int DV>
+__device__ inline void store_state_tiles(float *dst, const f32x4 (&S)[NTILE], uint32_t voff) {
+    const auto r = make_rsrc(dst, NTILE * 16 * DV * sizeof(float));
+#pragma unroll
+    for (int t = 0; t < NTILE; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_int(S[t][i]), r, (int)voff,
+                                                  (16 * t + i) * DV * (int)sizeof(float), 0);
+}
+
 constexpr int kScanPrefetch = 4;   // chunks of operands in flight ahead of the one computed
+
+// Runs step(chunk) over chunks 0 .. nch-1 with the operands of the next PF
+// chunks in flight, in a ring of PF + 1 operand sets.  The main loop is
+// unrolled over the ring so every ring index is a compile-time constant and
+// its body has no branch; a prefetch past the last chunk re-reads the last
+// one.  The final nch mod (PF + 1) chunks were prefetched by the main loop.
+template <int PF, typename Ops, typename Load, typename Step>
+__device__ inline void scan_ring(int nch, Load &load, Step &step, Ops *) {
+    constexpr int NB = PF + 1;
+    if (nch <= 0) return;
+    Ops ops[NB];
+#pragma unroll
+    for (int u = 0; u < PF; ++u) load(ops[u], min(u, nch - 1));
+    int j = 0;
+    for (; j + NB <= nch; j += NB) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            load(ops[(u + PF) % NB], min(j + u + PF, nch - 1));
+            step(ops[u], j + u);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < NB - 1; ++u)
+        if (j + u < nch) step(ops[u], j + u);
+}
 
 template <int DK> struct ScanGeom {
     static constexpr int NW = DK / 32;      // waves per workgroup (32 state rows each)
@@ -71,8 +128,8 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
     const int H = a.n_heads;
     if (pair >= a.n_seqs * H) return;
     const int seq = pair / H, h = pair % H;
-    const int64_t cu0 = a.cu[seq], len = (int64_t)a.cu[seq + 1] - cu0;
-    const int64_t nch = n_chunks32((int)len, a.C, a.cps);
+    const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
+    const int nch = n_chunks32(len, a.C, a.cps);
     const int64_t base = slot_base(cu0, seq, a.C, a.cps);
     const size_t state_off = (size_t)pair * DK * DV;
     const int col = 16 * tile + c16;
@@ -89,11 +146,9 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
         S[0] = zero4();
         S[1] = zero4();
     }
-    // Running chunk bounds (the plan of chunk_range, advanced by additions
-    // only: no 64-bit division in the loop).  A chunk ends at the next
-    // multiple of C, 64 tokens after its start, or at the end of the call.
-    int64_t pos = 0, next_ck = a.C;
-    int64_t ckpt_row = a.ckpt ? (int64_t)a.ckpt_off[seq] : 0;
+    ChunkCursor cur{0, a.C, len, a.C};
+    int ckpt_row = a.ckpt ? a.ckpt_off[seq] : 0;
+    const uint32_t lane_off = 4u * (uint32_t)(4 * g16 * DV + col);   // C-layout store offset
     // Drain the counters once here: without it the waitcnt pass sees the
     // state loads as possibly pending at the loop header and waits on the
     // in-flight operand prefetch in every iteration.
@@ -106,7 +161,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
         float gl;             // G_63
     };
     const uint32_t lane16 = 16u * (uint32_t)lane;
-    auto load = [&](Ops &o, int64_t jj) {
+    auto load = [&](Ops &o, int jj) {
         const int64_t sh = (base + jj) * H + h;
         // issue order: gate, U~, -W, K~^T (earliest-needed last is fine: each
         // use waits only for the loads issued before it)
@@ -129,7 +184,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
             for (int v = 0; v < VU; ++v) o.kt[t][v] = buf_load16(rk, lane16, 1024u * ((2 * w + t) * VU + v));
     };
 
-    auto step = [&](const Ops &o, int64_t j) {
+    auto step = [&](const Ops &o, int j) {
         const int64_t sh = (base + j) * H + h;
         // state entering the chunk as B operand over this wave's dk slice
         T sb[FW];
@@ -194,59 +249,27 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
             S[t] = acc;
         }
         // checkpoint when the chunk ends on a multiple of C
-        int64_t hi = pos + kChunk;
-        if (hi > next_ck) hi = next_ck;
-        if (hi > len) hi = len;
-        pos = hi;
-        if (hi == next_ck) {
-            next_ck += a.C;
-            const int64_t row = ckpt_row++;
-            if (a.ckpt) {
-                float *dst = a.ckpt + ((size_t)row * H + h) * DK * DV;
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        dst[(size_t)(32 * w + 16 * t + 4 * g16 + i) * DV + col] = S[t][i];
-            }
+        if (cur.advance()) {
+            const int row = ckpt_row++;
+            if (a.ckpt)
+                store_state_tiles<2, DV>(a.ckpt + ((size_t)row * H + h) * DK * DV + (size_t)32 * w * DV, S,
+                                         lane_off);
         }
     };
 
     // Operand ring: chunk j computes while chunks j + 1 .. j + kScanPrefetch
     // are in flight.  Operands come from MALL/HBM (each kernel starts with
-    // cold L2s), so several chunks of latency must be covered.  The inner
-    // loop is fully unrolled so every ring index is a compile-time constant.
-    constexpr int PF = kScanPrefetch, NB = PF + 1;
-    Ops ops[NB];
-    auto clampj = [&](int64_t jj) { return jj < nch ? jj : nch - 1; };
-    if (nch > 0) {
-#pragma unroll
-        for (int u = 0; u < PF; ++u) load(ops[u], clampj(u));
-    }
-    for (int64_t j = 0; j < nch; j += NB) {
-#pragma unroll
-        for (int u = 0; u < NB; ++u) {
-            if (j + u < nch) {
-                load(ops[(u + PF) % NB], clampj(j + u + PF));
-                step(ops[u], j + u);
-            }
-        }
-    }
+    // cold L2s), so several chunks of latency must be covered.
+    scan_ring<kScanPrefetch>(nch, load, step, (Ops *)nullptr);
 
-    if (a.final_state) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                a.final_state[state_off + (size_t)(32 * w + 16 * t + 4 * g16 + i) * DV + col] = S[t][i];
-    }
+    if (a.final_state) store_state_tiles<2, DV>(a.final_state + state_off + (size_t)32 * w * DV, S, lane_off);
 }
 
 
 // Single-wave form: one wave owns a 16-column tile and all DK state rows, so
 // a chunk needs no workgroup synchronisation: 4 * DK/32 MFMAs for U = U~ - W S
-// and 2 * DK/16 for the state update, with the chunk operands double-buffered
-// in registers.  Used where the sequential chain, not the operand bandwidth,
+// and 2 * DK/16 for the state update, with the operands of the next chunk in
+// flight while one is computed.  Used where the sequential chain, not the operand bandwidth,
 // bounds the scan (few sequence-head pairs).
 template <typename T, int DK, int DV>
 __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
@@ -258,6 +281,8 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
     constexpr int FS = DK / 4;              // per-lane operand values over dk
     constexpr int FU = kChunk / 4;          // per-lane operand values over chunk rows
     constexpr int VS = FS / VEC, VU = FU / VEC;
+    constexpr int kMfmas = 4 * (FS / KW) + RT * (FU / KW);   // per chunk
+    constexpr int kLoads = 1 + 4 + 4 * VS + RT * VU;          // operand loads per chunk
 
     const int lane = threadIdx.x, g16 = lane >> 4, c16 = lane & 15;
     const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
@@ -265,8 +290,8 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
     const int H = a.n_heads;
     if (pair >= a.n_seqs * H) return;
     const int seq = pair / H, h = pair % H;
-    const int64_t cu0 = a.cu[seq], len = (int64_t)a.cu[seq + 1] - cu0;
-    const int64_t nch = n_chunks32((int)len, a.C, a.cps);
+    const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
+    const int nch = n_chunks32(len, a.C, a.cps);
     const int64_t base = slot_base(cu0, seq, a.C, a.cps);
     const size_t state_off = (size_t)pair * DK * DV;
     const int col = 16 * tile + c16;
@@ -281,8 +306,9 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
 #pragma unroll
         for (int t = 0; t < RT; ++t) S[t] = zero4();
     }
-    int64_t pos = 0, next_ck = a.C;
-    int64_t ckpt_row = a.ckpt ? (int64_t)a.ckpt_off[seq] : 0;
+    ChunkCursor cur{0, a.C, len, a.C};
+    int ckpt_row = a.ckpt ? a.ckpt_off[seq] : 0;
+    const uint32_t lane_off = 4u * (uint32_t)(4 * g16 * DV + col);
     __builtin_amdgcn_s_waitcnt(0);   // see gdr_scan_kernel
 
     struct Ops {
@@ -292,7 +318,7 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
         uint4 kt[RT][VU];
     };
     const uint32_t lane16 = 16u * (uint32_t)lane;
-    auto load = [&](Ops &o, int64_t jj) {
+    auto load = [&](Ops &o, int jj) {
         const int64_t sh = (base + jj) * H + h;
         o.gl = buf_load4f(make_rsrc(a.ws.g + sh * kChunk, kChunk * sizeof(float)), 0u, 4u * (kChunk - 1));
         const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
@@ -312,7 +338,7 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
 #pragma unroll
             for (int v = 0; v < VU; ++v) o.kt[t][v] = buf_load16(rk, lane16, 1024u * (t * VU + v));
     };
-    auto step = [&](const Ops &o, int64_t j) {
+    auto step = [&](const Ops &o, int j) {
         const int64_t sh = (base + j) * H + h;
         T sb[FS];
 #pragma unroll
@@ -352,40 +378,25 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
                 acc = M::mma(M::pack(&kv[ks * KW]), M::pack(&ub[ks * KW]), acc);
             S[t] = acc;
         }
-        int64_t hi = pos + kChunk;
-        if (hi > next_ck) hi = next_ck;
-        if (hi > len) hi = len;
-        pos = hi;
-        if (hi == next_ck) {
-            next_ck += a.C;
-            const int64_t row = ckpt_row++;
-            if (a.ckpt) {
-                float *dst = a.ckpt + ((size_t)row * H + h) * DK * DV;
+        // One wave issues both the MFMA chain and the next chunk's operand
+        // loads (issued just before this step, in the same scheduling
+        // region).  Back to back, the loads stall the in-order issue on the
+        // memory pipeline while the matrix core idles; one load per MFMA
+        // keeps both busy.
 #pragma unroll
-                for (int t = 0; t < RT; ++t)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) dst[(size_t)(16 * t + 4 * g16 + i) * DV + col] = S[t][i];
-            }
+        for (int i = 0; i < kMfmas; ++i) {
+            if (i < kLoads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                   // MFMA
+        }
+        if (kLoads > kMfmas) __builtin_amdgcn_sched_group_barrier(0x020, kLoads - kMfmas, 0);
+        if (cur.advance()) {
+            const int row = ckpt_row++;
+            if (a.ckpt) store_state_tiles<RT, DV>(a.ckpt + ((size_t)row * H + h) * DK * DV, S, lane_off);
         }
     };
 
-    Ops o0, o1;
-    if (nch > 0) load(o0, 0);
-    for (int64_t j = 0; j < nch; j += 2) {
-        load(o1, j + 1 < nch ? j + 1 : j);
-        step(o0, j);
-        if (j + 1 < nch) {
-            load(o0, j + 2 < nch ? j + 2 : j + 1);
-            step(o1, j + 1);
-        }
-    }
-    if (a.final_state) {
-#pragma unroll
-        for (int t = 0; t < RT; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                a.final_state[state_off + (size_t)(16 * t + 4 * g16 + i) * DV + col] = S[t][i];
-    }
+    scan_ring<1>(nch, load, step, (Ops *)nullptr);
+    if (a.final_state) store_state_tiles<RT, DV>(a.final_state + state_off, S, lane_off);
 }
 
 }  // namespace la

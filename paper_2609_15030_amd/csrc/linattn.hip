@@ -44,13 +44,16 @@ constexpr size_t kRegionAlign = 256;
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Scan kernel form: 1 = one wave per 16-column tile, 4 = DK/32 waves sharing
-// the tile's state rows.  LA_SCAN_WAVES overrides the default (for tuning).
-int scan_variant() {
-    static const int v = [] {
+// the tile's state rows.  The single-wave form has the shorter chain; with
+// fp32 operands at dk = 128 it does not fit the register file, so that case
+// splits dk.  LA_SCAN_WAVES=1|4 overrides the choice (for tuning).
+int scan_variant(bool f32, int dk) {
+    static const int forced = [] {
         const char *e = getenv("LA_SCAN_WAVES");
-        return (e && atoi(e) == 4) ? 4 : 1;
+        return e ? atoi(e) : 0;
     }();
-    return v;
+    if (forced == 1 || forced == 4) return forced;
+    return (f32 && dk == 128) ? 4 : 1;
 }
 
 size_t io_size(int32_t dtype) { return dtype == LA_BF16 ? 2 : 4; }
@@ -143,7 +146,7 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
         constexpr int NT = DV / 16;
         const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
         const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
-        if (scan_variant() == 1)
+        if (scan_variant(sizeof(T) == 4, DK) == 1)
             hipLaunchKernelGGL((la::gdr_scan1_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(64), 0,
                                c.stream, sa);
         else
