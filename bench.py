@@ -79,6 +79,40 @@ def flops_per_token_head(dk, dv, L=CHUNK):
             "out": 2 * dk * dv + L * dk + L * dv}
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "prefill_tp_rank_T3584_hbm_counters.md")
+SCAN_SOURCES = ["paper_2609_15030_amd/csrc/la_common.h", "paper_2609_15030_amd/csrc/gdr_scan.h",
+                "paper_2609_15030_amd/csrc/linattn.hip", "paper_2609_15030_amd/build.py"]
+
+
+def scan_kernel_name(io_bf16, dk):
+    """The scan form the library launches (its default choice, or LA_SCAN_WAVES)."""
+    forced = os.environ.get("LA_SCAN_WAVES", "")
+    waves = int(forced) if forced in ("1", "4") else (4 if (not io_bf16 and dk == 128) else 1)
+    return "gdr_scan1_kernel" if waves == 1 else "gdr_scan_kernel"
+
+
+def measured_traffic(kernel):
+    """HBM bytes per cold launch of ``kernel`` from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None when the scan sources have changed
+    since the counters were taken (or no record exists)."""
+    import hashlib
+    try:
+        line = next(l for l in open(TRAFFIC_PROFILE) if l.startswith("traffic-record: "))
+    except (OSError, StopIteration):
+        return None
+    rec = json.loads(line[len("traffic-record: "):])
+    h = hashlib.sha256()
+    for f in SCAN_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if rec.get("source_sha256") != h.hexdigest():
+        return None
+    for r in rec["records"]:
+        if r["kernel"] == kernel and r["role"] == "cold":
+            return r["read_bytes"] + r["write_bytes"]
+    return None
+
+
 def cpu_baseline(w, B, seconds):
     """The fp64 oracle on the same workload (cold prefill + resume), repeated
     until about ``seconds`` of CPU time; threads over heads."""
@@ -218,10 +252,11 @@ def main():
     dom = max(stage_us, key=stage_us.get)
     achieved = fl[dom] * N * H / (stage_us[dom] * 1e-6) / 1e12
     prefill_us = sum(stage_us.values())
-    roofline = {"bound": "mfma", "kernel": {"prep": "gdr_prep_kernel", "scan": "gdr_scan_kernel",
-                                             "out": "gdr_out_kernel"}[dom],
+    kname = {"prep": "gdr_prep_kernel", "scan": scan_kernel_name(True, dk), "out": "gdr_out_kernel"}[dom]
+    roofline = {"bound": "mfma", "kernel": kname,
                 "achieved": round(achieved, 3), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / BF16_PEAK_TFLOPS, 5), "traffic": None,
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 5), "traffic": measured_traffic(kname),
+                "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)",
                 "flops_per_launch": fl[dom] * N * H, "avg_launch_us": round(stage_us[dom], 2)}
 
     out = {
