@@ -25,6 +25,19 @@
 
 namespace la {
 
+// Two-level scan, per segment slot and head (a segment is seg_m consecutive
+// chunks of one sequence; seg_m divides the chunks per checkpoint interval,
+// so every checkpoint position is a segment boundary).  Over a segment the
+// state map is affine: S_out = D S_in + Phi' S_in + R, with D the product of
+// the chunk decays, Phi' (dk x dk) the rest of the linear part and R
+// (dk x dv) the offset.
+struct SegWorkspace {
+    void *phi;        // Phi' in the io type, [DK][DK], columns in A-operand order
+    float *r;         // R, fp32, C-layout tiles [DV/16][DK/16][64 lanes][4]
+    float *d;         // D, fp32, one value per segment slot and head
+    float *state;     // state entering the segment, fp32 C-layout tiles (segments >= 1)
+};
+
 struct ScanArgs {
     const int32_t *cu;
     const float *state_in;        // [n_seqs, H, DK, DV] or null (zero state)
@@ -33,6 +46,8 @@ struct ScanArgs {
     const int32_t *ckpt_off;      // [n_seqs]
     int32_t n_seqs, n_heads, C, cps;
     Workspace ws;
+    int32_t seg_m, max_seg;       // two-level scan only
+    SegWorkspace seg;
 };
 
 // Chunk bounds of one sequence, advanced by additions only (the plan of
@@ -65,6 +80,54 @@ __device__ inline void store_state_tiles(float *dst, const f32x4 (&S)[NTILE], ui
         for (int i = 0; i < 4; ++i)
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_int(S[t][i]), r, (int)voff,
                                                   (16 * t + i) * DV * (int)sizeof(float), 0);
+}
+
+// Row-major store of NTILE 16-row tiles of one 16-column state tile through a
+// per-wave LDS transpose: each lane writes 16 bytes (4 consecutive columns of
+// one row) per store instead of one dword per row, so a [DK, 16] tile takes
+// DK/16 vector stores.  dst points at (row 0, the tile's first column) of a
+// row-major block with DV columns; lds holds NTILE * 16 * kTrLd floats owned
+// by this wave (the padded row keeps the 16-byte reads aligned and the
+// column writes conflict-free).
+constexpr int kTrLd = 20;
+
+template <int NTILE, int DV>
+__device__ inline void store_state_tiles_t(float *dst, const f32x4 (&S)[NTILE], float *lds) {
+    const int lane = threadIdx.x & 63, g16 = lane >> 4, c16 = lane & 15;
+#pragma unroll
+    for (int t = 0; t < NTILE; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) lds[(16 * t + 4 * g16 + i) * kTrLd + c16] = S[t][i];
+    const auto r = make_rsrc(dst, (uint32_t)(((NTILE * 16 - 1) * DV + 16) * sizeof(float)));
+    const int rr = lane >> 2, cc = 4 * (lane & 3);
+    const uint32_t voff = (uint32_t)((rr * DV + cc) * sizeof(float));
+#pragma unroll
+    for (int p = 0; p < NTILE; ++p) {
+        const float4 v = *(const float4 *)&lds[(16 * p + rr) * kTrLd + cc];
+        buf_store16(make_uint4(__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)),
+                    r, voff, (uint32_t)(16 * p * DV * sizeof(float)));
+    }
+}
+
+// State tiles in C layout ([tile][row tile][lane] of f32x4): the two-level
+// scan's segment-entering states, written by the combine and read by the
+// replay (one 16-byte access per row tile and lane).
+template <int RT>
+__device__ inline void store_state_c(float *base, int tile, const f32x4 (&S)[RT]) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+        ((float4 *)base)[(tile * RT + t) * 64 + lane] = make_float4(S[t][0], S[t][1], S[t][2], S[t][3]);
+}
+
+template <int RT>
+__device__ inline void load_state_c(const float *base, int tile, f32x4 (&S)[RT]) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int t = 0; t < RT; ++t) {
+        const float4 v = ((const float4 *)base)[(tile * RT + t) * 64 + lane];
+        S[t] = f32x4{v.x, v.y, v.z, v.w};
+    }
 }
 
 constexpr int kScanPrefetch = 4;   // chunks of operands in flight ahead of the one computed
@@ -266,50 +329,35 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
 }
 
 
-// Single-wave form: one wave owns a 16-column tile and all DK state rows, so
-// a chunk needs no workgroup synchronisation: 4 * DK/32 MFMAs for U = U~ - W S
-// and 2 * DK/16 for the state update, with the operands of the next chunk in
-// flight while one is computed.  Used where the sequential chain, not the operand bandwidth,
-// bounds the scan (few sequence-head pairs).
+// Single-wave form.  One wave owns a 16-column tile of the state and all DK
+// rows, kept in fp32 MFMA result registers, so a chunk needs no workgroup
+// synchronisation: 4 * DK/32 MFMAs for U = U~ - W S and 2 * DK/16 for the
+// state update, with the next chunk's operands in flight while one is
+// computed.  scan1_chunks runs the whole sequence of one (sequence, head) on
+// one tile: it hands the output kernel the state entering each chunk and U,
+// and writes the checkpoints.
 template <typename T, int DK, int DV>
-__global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
+__device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile, int len, int64_t base,
+                                    int nch, f32x4 (&S)[DK / 16]) {
     using M = MT<T>;
     using L = WsLayout<T, DK, DV>;
     constexpr int KW = M::KW, VEC = Vec<T>::N;
     constexpr int RT = DK / 16;             // state row tiles
-    constexpr int NT = DV / 16;             // waves per (sequence, head)
     constexpr int FS = DK / 4;              // per-lane operand values over dk
     constexpr int FU = kChunk / 4;          // per-lane operand values over chunk rows
     constexpr int VS = FS / VEC, VU = FU / VEC;
-    constexpr int kMfmas = 4 * (FS / KW) + RT * (FU / KW);   // per chunk
-    constexpr int kLoads = 1 + 4 + 4 * VS + RT * VU;          // operand loads per chunk
+    constexpr int kMfmas = 4 * (FS / KW) + RT * (FU / KW);       // per chunk
+    constexpr int kLoads = 1 + 4 + 4 * VS + RT * VU;              // operand loads per chunk
 
-    const int lane = threadIdx.x, g16 = lane >> 4, c16 = lane & 15;
-    const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
-    const int pair = xcd + 8 * (q / NT), tile = q % NT;
+    const int lane = threadIdx.x & 63, g16 = lane >> 4, c16 = lane & 15;
     const int H = a.n_heads;
-    if (pair >= a.n_seqs * H) return;
-    const int seq = pair / H, h = pair % H;
-    const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
-    const int nch = n_chunks32(len, a.C, a.cps);
-    const int64_t base = slot_base(cu0, seq, a.C, a.cps);
-    const size_t state_off = (size_t)pair * DK * DV;
-    const int col = 16 * tile + c16;
-
-    f32x4 S[RT];
-    if (a.state_in) {
-#pragma unroll
-        for (int t = 0; t < RT; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) S[t][i] = a.state_in[state_off + (size_t)(16 * t + 4 * g16 + i) * DV + col];
-    } else {
-#pragma unroll
-        for (int t = 0; t < RT; ++t) S[t] = zero4();
-    }
     ChunkCursor cur{0, a.C, len, a.C};
     int ckpt_row = a.ckpt ? a.ckpt_off[seq] : 0;
-    const uint32_t lane_off = 4u * (uint32_t)(4 * g16 * DV + col);
-    __builtin_amdgcn_s_waitcnt(0);   // see gdr_scan_kernel
+    const uint32_t lane_off = 4u * (uint32_t)(4 * g16 * DV + 16 * tile + c16);
+    // Drain the counters once here: without it the waitcnt pass sees the
+    // state loads as possibly pending at the loop header and waits on the
+    // in-flight operand prefetch in every iteration.
+    __builtin_amdgcn_s_waitcnt(0);
 
     struct Ops {
         float gl;
@@ -338,8 +386,8 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
 #pragma unroll
             for (int v = 0; v < VU; ++v) o.kt[t][v] = buf_load16(rk, lane16, 1024u * (t * VU + v));
     };
-    auto step = [&](const Ops &o, int j) {
-        const int64_t sh = (base + j) * H + h;
+    auto step = [&](const Ops &o, int jj) {
+        const int64_t sh = (base + jj) * H + h;
         T sb[FS];
 #pragma unroll
         for (int f = 0; f < FS; ++f) sb[f] = from_f32<T>(S[f >> 2][f & 3]);
@@ -394,9 +442,137 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
             if (a.ckpt) store_state_tiles<RT, DV>(a.ckpt + ((size_t)row * H + h) * DK * DV, S, lane_off);
         }
     };
-
     scan_ring<1>(nch, load, step, (Ops *)nullptr);
-    if (a.final_state) store_state_tiles<RT, DV>(a.final_state + state_off, S, lane_off);
+}
+
+// Loads a [DK][DV] fp32 state's tile into C layout (or zeros for null).
+template <int DK, int DV>
+__device__ inline void load_state_tile(const float *src, int tile, f32x4 (&S)[DK / 16]) {
+    const int lane = threadIdx.x & 63, g16 = lane >> 4, col = 16 * tile + (lane & 15);
+    if (src) {
+#pragma unroll
+        for (int t = 0; t < DK / 16; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) S[t][i] = src[(size_t)(16 * t + 4 * g16 + i) * DV + col];
+    } else {
+#pragma unroll
+        for (int t = 0; t < DK / 16; ++t) S[t] = zero4();
+    }
+}
+
+// Whole-sequence scan: one wave per (sequence, head, 16-column tile).  The
+// NT waves of one (sequence, head) land on one XCD (workgroups are dealt to
+// the 8 XCDs round-robin) and share the chunk operands through its L2.
+template <typename T, int DK, int DV>
+__global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
+    constexpr int NT = DV / 16;
+    const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
+    const int pair = xcd + 8 * (q / NT), tile = q % NT;
+    const int H = a.n_heads;
+    if (pair >= a.n_seqs * H) return;
+    const int seq = pair / H, h = pair % H;
+    const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
+    const int nch = n_chunks32(len, a.C, a.cps);
+    const int64_t base = slot_base(cu0, seq, a.C, a.cps);
+    const size_t state_off = (size_t)pair * DK * DV;
+    f32x4 S[DK / 16];
+    load_state_tile<DK, DV>(a.state_in ? a.state_in + state_off : nullptr, tile, S);
+    scan1_chunks<T, DK, DV>(a, seq, h, tile, len, base, nch, S);
+    if (a.final_state) {
+        const int lane = threadIdx.x;
+        store_state_tiles<DK / 16, DV>(a.final_state + state_off, S,
+                                       4u * (uint32_t)(4 * (lane >> 4) * DV + 16 * tile + (lane & 15)));
+    }
+}
+
+// Position in the A-operand column order of column c of a [DK][DK] matrix:
+// A-operand k-step ks of a lane in group g takes columns perm_row(8 ks + j, g)
+// for j < 8, stored contiguously at 32 ks + 8 g + j.
+__device__ inline int phi_col_pos(int c) {
+    const int t = c >> 4, g = (c >> 2) & 3, q = c & 3;
+    return 32 * (t >> 1) + 8 * g + 4 * (t & 1) + q;
+}
+
+// Two-level scan, second level: per (sequence, head, 16-column tile), the
+// segment states in order, S <- D S + Phi' S + R.  The large D I part stays
+// in fp32; only Phi' S goes through the io-type MFMA.  Writes the
+// checkpoints (segment ends on a multiple of C), the entering state of every
+// later segment, and the final state.
+template <typename T, int DK, int DV>
+__global__ __launch_bounds__(64) void gdr_seg_combine_kernel(ScanArgs a) {
+    using M = MT<T>;
+    constexpr int KW = M::KW, VEC = Vec<T>::N;
+    constexpr int RT = DK / 16, NT = DV / 16;
+    constexpr int FS = DK / 4, VS = FS / VEC;
+    constexpr int kMfmas = RT * (FS / KW), kLoads = 1 + RT + RT * VS;
+    const int lane = threadIdx.x, g16 = lane >> 4, c16 = lane & 15;
+    const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
+    const int pair = xcd + 8 * (q / NT), tile = q % NT;
+    const int H = a.n_heads;
+    if (pair >= a.n_seqs * H) return;
+    const int seq = pair / H, h = pair % H;
+    const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
+    const int nch = n_chunks32(len, a.C, a.cps);
+    const int nseg = (nch + a.seg_m - 1) / a.seg_m;
+    const int64_t sbase = slot_base(cu0, seq, (int64_t)a.C * a.seg_m, a.cps);
+    const size_t state_off = (size_t)pair * DK * DV;
+    __shared__ float tr_lds[DK * kTrLd];
+    f32x4 S[RT];
+    load_state_tile<DK, DV>(a.state_in ? a.state_in + state_off : nullptr, tile, S);
+    const int ckpt0 = a.ckpt ? a.ckpt_off[seq] : 0;
+    const uint32_t lane16 = 16u * (uint32_t)lane;
+    const uint32_t phi_lane = (uint32_t)((c16 * DK + 8 * g16) * sizeof(T));
+    __builtin_amdgcn_s_waitcnt(0);
+
+    struct Ops {
+        float d;
+        f32x4 r[RT];
+        uint4 ph[RT][VS];
+    };
+    auto load = [&](Ops &o, int sg) {
+        const int64_t ssh = (sbase + sg) * H + h;
+        o.d = buf_load4f(make_rsrc(a.seg.d + ssh, sizeof(float)), 0u, 0u);
+        const auto rr = make_rsrc(a.seg.r + ssh * DK * DV, DK * DV * sizeof(float));
+#pragma unroll
+        for (int t = 0; t < RT; ++t) {
+            const uint4 x = buf_load16(rr, lane16, 1024u * (tile * RT + t));
+            o.r[t] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
+        }
+        const auto rp = make_rsrc((const T *)a.seg.phi + ssh * DK * DK, DK * DK * sizeof(T));
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+            for (int v = 0; v < VS; ++v)
+                o.ph[t][v] = buf_load16(rp, phi_lane, (uint32_t)((16 * t * DK + v * VEC * 4) * sizeof(T)));
+    };
+    auto step = [&](const Ops &o, int sg) {
+        T sb[FS];
+#pragma unroll
+        for (int f = 0; f < FS; ++f) sb[f] = from_f32<T>(S[f >> 2][f & 3]);
+#pragma unroll
+        for (int t = 0; t < RT; ++t) {
+            const T *pv = (const T *)&o.ph[t][0];
+            f32x4 acc = S[t] * o.d + o.r[t];
+#pragma unroll
+            for (int ks = 0; ks < FS / KW; ++ks)
+                acc = M::mma(M::pack(&pv[ks * KW]), M::pack(&sb[ks * KW]), acc);
+            S[t] = acc;
+        }
+#pragma unroll
+        for (int i = 0; i < kMfmas; ++i) {
+            if (i < kLoads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+        if (kLoads > kMfmas) __builtin_amdgcn_sched_group_barrier(0x020, kLoads - kMfmas, 0);
+        int lo, hi;
+        chunk_range32(min((sg + 1) * a.seg_m, nch) - 1, len, a.C, a.cps, &lo, &hi);
+        if (sg + 1 < nseg) store_state_c<RT>(a.seg.state + ((sbase + sg + 1) * H + h) * DK * DV, tile, S);
+        if (hi % a.C == 0 && a.ckpt)
+            store_state_tiles_t<RT, DV>(a.ckpt + ((size_t)(ckpt0 + hi / a.C - 1) * H + h) * DK * DV + 16 * tile, S,
+                                        tr_lds);
+    };
+    scan_ring<1>(nseg, load, step, (Ops *)nullptr);
+    if (a.final_state) store_state_tiles_t<RT, DV>(a.final_state + state_off + 16 * tile, S, tr_lds);
 }
 
 }  // namespace la

@@ -14,6 +14,7 @@
 #include "la_common.h"
 #include "gdr_prep.h"
 #include "gdr_scan.h"
+#include "gdr_group.h"
 #include "gdr_out.h"
 #include "paged.h"
 
@@ -58,6 +59,29 @@ int scan_variant(bool f32, int dk) {
 
 size_t io_size(int32_t dtype) { return dtype == LA_BF16 ? 2 : 4; }
 
+// Chunks per segment of the two-level scan (1 = single-level).  A segment
+// must divide a checkpoint interval's chunks, so every checkpoint position is
+// a segment boundary and a resume from a checkpoint sees the same segments
+// (and computes bit-identical states) as the run that wrote it; for the same
+// reason the choice depends on the interval only, never on the lengths.  The
+// largest such divisor up to 16 balances the two parallel levels against the
+// sequential combine.  Intervals of fewer than 8 chunks keep the
+// single-level scan: there a segment's map costs more than the chunks it
+// replaces.  bf16 operands only.  LA_SCAN_LEVELS=1|2 forces one form (for
+// tuning).
+int seg_chunks(const la_shape *s) {
+    static const int forced = [] {
+        const char *e = getenv("LA_SCAN_LEVELS");
+        return e ? atoi(e) : 0;
+    }();
+    if (forced == 1 || s->io_dtype != LA_BF16) return 1;
+    const int cps = la::chunks_per_interval(s->ckpt_interval);
+    if (forced != 2 && cps < 8) return 1;
+    for (int m = std::min(cps, 16); m >= 2; --m)
+        if (cps % m == 0) return m;
+    return 1;
+}
+
 bool shape_supported(const la_shape *s) {
     return (s->dk == 64 || s->dk == 128) && (s->dv == 64 || s->dv == 128) && s->chunk == la::kChunk;
 }
@@ -79,7 +103,10 @@ la_status check_shape(const la_shape *s) {
 }
 
 struct WsPlan {
-    size_t w, kt, ut, g, sc, u, total;   // byte offsets of each region, total size
+    size_t w, kt, ut, g, sc, u;              // byte offsets of each region
+    size_t phi, segr, segd, segst;           // two-level scan regions (seg_m >= 2)
+    int seg_m;
+    size_t total;
 };
 
 WsPlan plan_workspace(const la_shape *s, int64_t total_tokens) {
@@ -96,6 +123,16 @@ WsPlan plan_workspace(const la_shape *s, int64_t total_tokens) {
     p.g = take(sh * la::kChunk * sizeof(float));
     p.sc = take(sh * (size_t)s->dk * s->dv * io);
     p.u = take(sh * la::kChunk * s->dv * io);
+    p.seg_m = seg_chunks(s);
+    p.phi = p.segr = p.segd = p.segst = 0;
+    if (p.seg_m > 1) {
+        const int64_t seg_slots = la::total_slots(total_tokens, s->n_seqs, s->ckpt_interval * (int64_t)p.seg_m, cps);
+        const size_t ssh = (size_t)seg_slots * s->n_heads;
+        p.phi = take(ssh * s->dk * s->dk * io);
+        p.segr = take(ssh * s->dk * s->dv * sizeof(float));
+        p.segd = take(ssh * sizeof(float));
+        p.segst = take(ssh * s->dk * s->dv * sizeof(float));
+    }
     p.total = std::max<size_t>(off, kRegionAlign);
     return p;
 }
@@ -114,6 +151,55 @@ struct PrefillCall {
     size_t ws_bytes;
     hipStream_t stream;
 };
+
+template <typename T, int DK, int DV>
+la_status launch_out(const PrefillCall &c, const la::Workspace &ws, int64_t max_chunks, bool trace) {
+    const la_shape *s = c.shape;
+    const int cps = la::chunks_per_interval(s->ckpt_interval);
+    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[2], c.stream);
+    if (max_chunks > 0) {
+        la::OutArgs oa{c.q, c.k, c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
+                       (int32_t)max_chunks, s->scale, ws};
+        const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
+        hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(256), 0, c.stream, oa);
+        if (la_status e = hip_check("output launch")) return e;
+    }
+    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[3], c.stream);
+    return LA_OK;
+}
+
+// Two-level scan: segment maps (all segments at once), the sequential
+// combine over segments, then every segment replayed from its entering
+// state; then the output kernel.
+template <typename T, int DK, int DV>
+la_status launch_two_level(const PrefillCall &c, const WsPlan &p, la::ScanArgs sa, int64_t max_chunks,
+                           bool trace) {
+    const la_shape *s = c.shape;
+    char *base = (char *)c.workspace;
+    sa.seg_m = p.seg_m;
+    sa.max_seg = (int32_t)((max_chunks + p.seg_m - 1) / p.seg_m);
+    sa.seg.phi = base + p.phi;
+    sa.seg.r = (float *)(base + p.segr);
+    sa.seg.d = (float *)(base + p.segd);
+    sa.seg.state = (float *)(base + p.segst);
+    constexpr int NT = DV / 16;
+    const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
+    const int64_t units = pairs * sa.max_seg;
+    if (units > 0) {
+        hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupTrans>), dim3((unsigned)units),
+                           dim3(64 * la::kGroupWaves), 0, c.stream, sa);
+        if (la_status e = hip_check("segment map launch")) return e;
+    }
+    hipLaunchKernelGGL((la::gdr_seg_combine_kernel<T, DK, DV>), dim3((unsigned)(8 * NT * ((pairs + 7) / 8))),
+                       dim3(64), 0, c.stream, sa);
+    if (la_status e = hip_check("segment combine launch")) return e;
+    if (units > 0) {
+        hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupReplay>), dim3((unsigned)units),
+                           dim3(64 * la::kGroupWaves), 0, c.stream, sa);
+        if (la_status e = hip_check("segment replay launch")) return e;
+    }
+    return launch_out<T, DK, DV>(c, sa.ws, max_chunks, trace);
+}
 
 template <typename T, int DK, int DV>
 la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) {
@@ -142,10 +228,23 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[1], c.stream);
     {
         la::ScanArgs sa{c.cu_dev, c.state_in, c.final_state, c.ckpt_out, c.ckpt_off_dev,
-                        s->n_seqs, s->n_heads, s->ckpt_interval, cps, ws};
+                        s->n_seqs, s->n_heads, s->ckpt_interval, cps, ws, 1, 0, {}};
         constexpr int NT = DV / 16;
         const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
         const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
+        if constexpr (sizeof(T) == 2) {
+            if (p.seg_m > 1) return launch_two_level<T, DK, DV>(c, p, sa, max_chunks, trace);
+            static const bool group = [] {
+                const char *e = getenv("LA_SCAN_GROUP");
+                return e && atoi(e) == 1;
+            }();
+            if (group) {
+                hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupFull>), dim3((unsigned)pairs),
+                                   dim3(64 * la::kGroupWaves), 0, c.stream, sa);
+                if (la_status e = hip_check("inter-chunk scan launch")) return e;
+                return launch_out<T, DK, DV>(c, ws, max_chunks, trace);
+            }
+        }
         if (scan_variant(sizeof(T) == 4, DK) == 1)
             hipLaunchKernelGGL((la::gdr_scan1_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(64), 0,
                                c.stream, sa);
@@ -154,16 +253,7 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
                                dim3(64 * la::ScanGeom<DK>::NW), 0, c.stream, sa);
         if (la_status e = hip_check("inter-chunk scan launch")) return e;
     }
-    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[2], c.stream);
-    if (max_chunks > 0) {
-        la::OutArgs oa{c.q, c.k, c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
-                       (int32_t)max_chunks, s->scale, ws};
-        const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
-        hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(256), 0, c.stream, oa);
-        if (la_status e = hip_check("output launch")) return e;
-    }
-    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[3], c.stream);
-    return LA_OK;
+    return launch_out<T, DK, DV>(c, ws, max_chunks, trace);
 }
 
 template <typename T>
@@ -212,6 +302,12 @@ la_status run_prefill(const PrefillCall &c) {
     if (max_chunks > 0x7fffffff ||
         la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks) > 0x7fffffff)
         return fail(LA_ERR_INVALID_ARG, "sequence too long for one launch");
+    {
+        const int m = seg_chunks(s);
+        const int64_t units = (int64_t)s->n_seqs * s->n_heads * ((max_chunks + m - 1) / m);
+        if (m > 1 && units > 0x7fffffff)
+            return fail(LA_ERR_INVALID_ARG, "too many segments for one launch");
+    }
     if (total > 0) {
         if (!c.q || !c.k || !c.v || !c.g || !c.beta || !c.o)
             return fail(LA_ERR_INVALID_ARG, "q, k, v, g, beta and o are required");
@@ -237,6 +333,16 @@ la_status run_prefill(const PrefillCall &c) {
         const int64_t len = (int64_t)c.cu_host[i + 1] - c.cu_host[i];
         if (la::slot_base(c.cu_host[i], i, C, cps) + la::n_chunks(len, C, cps) > slots)
             return fail(LA_ERR_INVALID_ARG, "internal: chunk plan exceeds its workspace at sequence %d", i);
+    }
+    if (p.seg_m > 1) {
+        const int64_t K = C * p.seg_m;
+        const int64_t seg_slots = la::total_slots(total, s->n_seqs, K, cps);
+        for (int i = 0; i < s->n_seqs; ++i) {
+            const int64_t len = (int64_t)c.cu_host[i + 1] - c.cu_host[i];
+            const int64_t nseg = (la::n_chunks(len, C, cps) + p.seg_m - 1) / p.seg_m;
+            if (la::slot_base(c.cu_host[i], i, K, cps) + nseg > seg_slots)
+                return fail(LA_ERR_INVALID_ARG, "internal: segment plan exceeds its workspace at sequence %d", i);
+        }
     }
 
     if (s->io_dtype == LA_BF16) return dispatch_dims<__bf16>(c, p, max_chunks);

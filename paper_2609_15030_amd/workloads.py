@@ -136,8 +136,13 @@ def _normals(rng, shape, io_dtype, unit_rows):
 
 
 def draw(rng: np.random.Generator, seqlens, n_heads: int, dk: int, dv: int,
-         io_dtype: str) -> Inputs:
-    """Draw one packed input with the distributions stated in the module doc."""
+         io_dtype: str, gate_scale: float = 1.0) -> Inputs:
+    """Draw one packed input with the distributions stated in the module doc.
+
+    ``gate_scale`` multiplies the log-decay (g = -softplus(N(0, 1)) * scale,
+    in fp64 before rounding): 1 is the specified distribution, whose state
+    forgets everything older than a chunk (mean g = -0.81 per token); small
+    scales give long-memory inputs whose state is carried across many chunks."""
     seqlens = [int(n) for n in seqlens]
     T = int(sum(seqlens))
     q = _normals(rng, (T, n_heads, dk), io_dtype, True)
@@ -146,17 +151,17 @@ def draw(rng: np.random.Generator, seqlens, n_heads: int, dk: int, dv: int,
     b_logit = rng.standard_normal((T, n_heads))
     g_logit = rng.standard_normal((T, n_heads))
     beta = (1.0 / (1.0 + np.exp(-b_logit))).astype(np.float32)
-    g = (-np.logaddexp(0.0, g_logit)).astype(np.float32)
+    g = (-np.logaddexp(0.0, g_logit) * gate_scale).astype(np.float32)
     cu = np.zeros(len(seqlens) + 1, np.int32)
     cu[1:] = np.cumsum(seqlens)
     return Inputs(q, k, v, g, beta, cu, io_dtype)
 
 
 def random_inputs(seed: int, seqlens, n_heads: int, dk: int, dv: int,
-                  io_dtype: str = BF16) -> Inputs:
-    """Inputs for ad-hoc test shapes (edge cases, ragged tails)."""
+                  io_dtype: str = BF16, gate_scale: float = 1.0) -> Inputs:
+    """Inputs for ad-hoc test shapes (edge cases, ragged tails, long memory)."""
     return draw(np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed))),
-                seqlens, n_heads, dk, dv, io_dtype)
+                seqlens, n_heads, dk, dv, io_dtype, gate_scale)
 
 
 @dataclasses.dataclass
