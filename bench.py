@@ -12,6 +12,10 @@ checkpoint interval C = 256):
   4. paged restore of the 8 pages of the checkpoint at B;
   5. resume over the 256-token suffix [B, N) from the restored state.
 
+Beside the step it reports, each on its own timer: paged save/restore
+bandwidth on the full 4,096-page pool, and decode continuation (one token
+per sequence and head per call, state in HBM) at 1 and 64 sequences.
+
 Inputs are resident in HBM before timing starts.  The JSON line reports
 whole-step prefill tokens/s (3,584 + 256 tokens per step), the dominant
 kernel's roofline (per-kernel durations from HIP events recorded inside the
@@ -136,6 +140,32 @@ def cpu_baseline(w, B, seconds):
     return {"value": tokens / dt, "unit": "tokens/s", "cores": used, "kind": "oracle",
             "sample": f"{reps} x (cold prefill {N} tok + resume {N - B} tok) x {x.n_heads} heads, "
                       f"fp64 token loop, {dt:.1f} s wall"}
+
+
+def bench_decode(la, torch, stream_ptr, events, H, dk, dv, C, batches=(1, 64), steps=200):
+    """Decode continuation: one token per (sequence, head) per call, state read
+    and written in HBM (2 x 4 dk dv bytes per head-token)."""
+    out = {}
+    for n in batches:
+        shape = la.make_shape(n, H, dk, dv, C)
+        q = torch.randn((n, H, dk), device="cuda").to(torch.bfloat16)
+        k = torch.nn.functional.normalize(torch.randn((n, H, dk), device="cuda"), dim=-1).to(torch.bfloat16)
+        v = torch.randn((n, H, dv), device="cuda").to(torch.bfloat16)
+        g = -torch.nn.functional.softplus(torch.randn((n, H), device="cuda"))
+        beta = torch.sigmoid(torch.randn((n, H), device="cuda"))
+        state = torch.zeros((n, H, dk, dv), device="cuda")
+        o = torch.empty((n, H, dv), dtype=torch.bfloat16, device="cuda")
+        for _ in range(20):
+            la.la_decode_step(shape, q, k, v, g, beta, state, o)
+        events.record(4, stream_ptr)
+        for _ in range(steps):
+            la.la_decode_step(shape, q, k, v, g, beta, state, o)
+        events.record(5, stream_ptr)
+        us = events.ms(4, 5) / steps * 1e3
+        gbps = 2.0 * 4 * dk * dv * n * H / (us * 1e-6) / 1e9
+        out[f"{n}x{H}"] = {"us_per_step": round(us, 2), "tokens_per_s": round(n / (us * 1e-6), 1),
+                           "state_GBps": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)}
+    return out
 
 
 def bench_pool(la, torch, stream_ptr, events, n_pages=4096, page_elems=128 * 128, reps=20):
@@ -278,6 +308,7 @@ def main():
     }
     if not args.no_pool:
         out["save_restore"] = bench_pool(la, torch, sp, ev)
+    out["decode"] = bench_decode(la, torch, sp, ev, H, dk, dv, C)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, B, args.cpu_seconds)
     print(json.dumps(out), flush=True)

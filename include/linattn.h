@@ -157,6 +157,27 @@ la_status la_prefill_resume(const la_shape *shape,
                             void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * la_decode_step - decode continuation: advance every (sequence, head) by one
+ * generated token from its fp32 state (the recurrent state of section 2.1,
+ * continued after a cold prefill or a reload; sections 5.1, 5.4 and 5.5
+ * compare 64-, 256- and 128-token continuations).
+ *
+ * q, k: [n_seqs, H, dk]; v: [n_seqs, H, dv] in shape->io_dtype; g, beta:
+ * [n_seqs, H] fp32; state: [n_seqs, H, dk, dv] fp32, read and overwritten
+ * with the state after the token (16-byte aligned); o: [n_seqs, H, dv] in
+ * io_dtype, o = scale * S_new^T q.  The recurrence is the prefill's
+ * (shape->variant selects the prediction), token by token in fp32.
+ * shape->chunk and ckpt_interval are validated as for the prefill and
+ * otherwise unused.  All buffers device, caller-owned; outputs must not
+ * alias inputs other than state.  Errors: INVALID_ARG (NULL pointer,
+ * misaligned state), UNSUPPORTED (dk, dv outside {64, 128}), HIP.
+ */
+la_status la_decode_step(const la_shape *shape,
+                         const void *q, const void *k, const void *v,
+                         const float *g, const float *beta,
+                         float *state, void *o, void *stream);
+
+/*
  * la_state_save_paged - scatter states into a paged fp32 pool (the paper's
  * page rows, section 3.1 and Table 5; a save must complete before dependent
  * reuse, so order the reuse on the same stream or behind an event).

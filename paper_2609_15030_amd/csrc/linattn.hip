@@ -16,6 +16,7 @@
 #include "gdr_scan.h"
 #include "gdr_group.h"
 #include "gdr_out.h"
+#include "gdr_decode.h"
 #include "paged.h"
 
 namespace {
@@ -349,6 +350,22 @@ la_status run_prefill(const PrefillCall &c) {
     return dispatch_dims<float>(c, p, max_chunks);
 }
 
+template <typename T, int DK, int DV>
+la_status launch_decode(const la_shape *s, const la::DecodeArgs &a, hipStream_t stream) {
+    const int64_t blocks = (int64_t)s->n_seqs * s->n_heads * (DV / la::kDecodeCols);
+    hipLaunchKernelGGL((la::gdr_decode_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(la::kDecodeThreads), 0,
+                       stream, a);
+    return hip_check("decode launch");
+}
+
+template <typename T>
+la_status decode_dims(const la_shape *s, const la::DecodeArgs &a, hipStream_t stream) {
+    if (s->dk == 64 && s->dv == 64) return launch_decode<T, 64, 64>(s, a, stream);
+    if (s->dk == 64 && s->dv == 128) return launch_decode<T, 64, 128>(s, a, stream);
+    if (s->dk == 128 && s->dv == 64) return launch_decode<T, 128, 64>(s, a, stream);
+    return launch_decode<T, 128, 128>(s, a, stream);
+}
+
 la_status check_paged(const float *a, const float *b, int64_t n_items, int64_t page_elems, int64_t n_pages,
                       const int32_t *ids) {
     if (n_items < 0 || n_items > 0x7fffffff) return fail(LA_ERR_INVALID_ARG, "n_items=%lld", (long long)n_items);
@@ -402,6 +419,21 @@ la_status la_prefill_resume(const la_shape *shape, const void *q, const void *k,
                   state_in, o, final_state, ckpt_out, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
                   (hipStream_t)stream};
     return run_prefill(c);
+}
+
+la_status la_decode_step(const la_shape *shape, const void *q, const void *k, const void *v, const float *g,
+                         const float *beta, float *state, void *o, void *stream) {
+    if (la_status e = check_shape(shape)) return e;
+    if (!q || !k || !v || !g || !beta || !state || !o)
+        return fail(LA_ERR_INVALID_ARG, "q, k, v, g, beta, state and o are required");
+    if (!aligned16(state)) return fail(LA_ERR_INVALID_ARG, "state must be 16-byte aligned");
+    const size_t io = io_size(shape->io_dtype);
+    if ((uintptr_t)q % io || (uintptr_t)k % io || (uintptr_t)v % io || (uintptr_t)o % io)
+        return fail(LA_ERR_INVALID_ARG, "q, k, v and o must be aligned to their element size");
+    la::DecodeArgs a{q, k, v, g, beta, state, o, shape->n_seqs, shape->n_heads, shape->variant, shape->scale};
+    (void)hipGetLastError();
+    if (shape->io_dtype == LA_BF16) return decode_dims<__bf16>(shape, a, (hipStream_t)stream);
+    return decode_dims<float>(shape, a, (hipStream_t)stream);
 }
 
 la_status la_state_save_paged(const float *states, int64_t n_items, int64_t page_elems, float *pool,

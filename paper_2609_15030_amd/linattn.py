@@ -32,7 +32,7 @@ LA_GDR_LITERAL = 0
 LA_GDR_DECAYED_DELTA = 1
 
 EXPORTED = ("strict_prefix_boundary", "la_prefill_workspace_bytes", "la_prefill",
-            "la_prefill_resume", "la_state_save_paged", "la_state_restore_paged",
+            "la_prefill_resume", "la_decode_step", "la_state_save_paged", "la_state_restore_paged",
             "la_status_string", "la_last_error_message", "la_trace_set_events")
 
 
@@ -72,6 +72,7 @@ def _load() -> ctypes.CDLL:
         "la_prefill_workspace_bytes": ([SH, I64], SZ),
         "la_prefill": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_prefill_resume": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "la_decode_step": ([SH, P, P, P, P, P, P, P, P], I32),
         "la_state_save_paged": ([P, I64, I64, P, I64, P, P, P], I32),
         "la_state_restore_paged": ([P, I64, P, P, I64, I64, P, P], I32),
         "la_status_string": ([I32], ctypes.c_char_p),
@@ -207,6 +208,16 @@ def la_state_restore_paged(pool, page_ids_dev, states, err_count_dev=None, strea
     n_items = page_ids_dev.numel()
     st = _lib.la_state_restore_paged(_dptr(pool), n_pages, _dptr(page_ids_dev), _dptr(states),
                                      n_items, page_elems, _dptr(err_count_dev), _stream(stream))
+    if check:
+        _check(st)
+    return st
+
+
+def la_decode_step(shape: LaShape, q, k, v, g, beta, state, o, stream=None, check: bool = True) -> int:
+    """One decode token per (sequence, head): state [n_seqs, H, dk, dv] fp32 is
+    updated in place, o [n_seqs, H, dv] receives the output."""
+    st = _lib.la_decode_step(ctypes.byref(shape), _dptr(q), _dptr(k), _dptr(v), _dptr(g), _dptr(beta),
+                             _dptr(state), _dptr(o), _stream(stream))
     if check:
         _check(st)
     return st

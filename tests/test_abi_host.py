@@ -133,6 +133,24 @@ def test_paged_validation_before_launch():
     assert lib.la_state_save_paged(FAKE, 0, 8, FAKE, 8, FAKE, None, None) == la.LA_OK   # nothing to do
 
 
+def test_decode_validation_before_launch():
+    lib = la.library()
+    sh = la.make_shape(2, 8, 128, 128, 256)
+    ok = [FAKE] * 7
+    for i in range(7):                      # every buffer is required
+        args = list(ok)
+        args[i] = None
+        assert lib.la_decode_step(la.ctypes.byref(sh), *args, None) == la.LA_ERR_INVALID_ARG
+    # state misaligned; q misaligned for bf16
+    assert lib.la_decode_step(la.ctypes.byref(sh), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 4, FAKE,
+                              None) == la.LA_ERR_INVALID_ARG
+    assert lib.la_decode_step(la.ctypes.byref(sh), FAKE + 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                              None) == la.LA_ERR_INVALID_ARG
+    bad = la.make_shape(2, 8, 96, 128, 256)
+    assert lib.la_decode_step(la.ctypes.byref(bad), *ok, None) == la.LA_ERR_UNSUPPORTED
+    assert lib.la_decode_step(None, *ok, None) == la.LA_ERR_INVALID_ARG
+
+
 def test_status_strings():
     assert la.status_string(la.LA_ERR_EMPTY_SUFFIX) == "LA_ERR_EMPTY_SUFFIX"
     assert la.status_string(99) == "LA_ERR_UNKNOWN"
