@@ -13,8 +13,10 @@ checkpoint interval C = 256):
   5. resume over the 256-token suffix [B, N) from the restored state.
 
 Beside the step it reports, each on its own timer: paged save/restore
-bandwidth on the full 4,096-page pool, and decode continuation (one token
-per sequence and head per call, state in HBM) at 1 and 64 sequences.
+bandwidth on the full 4,096-page pool, decode continuation (one token per
+sequence and head per call, state in HBM) at 1 and 64 sequences, and the
+host-memory tier (pages to and from a pinned host pool) for the 112
+checkpoint pages of a step and for 4,096 pages.
 
 Inputs are resident in HBM before timing starts.  The JSON line reports
 whole-step prefill tokens/s (3,584 + 256 tokens per step), the dominant
@@ -168,6 +170,35 @@ def bench_decode(la, torch, stream_ptr, events, H, dk, dv, C, batches=(1, 64), s
     return out
 
 
+def bench_host_tier(la, torch, stream_ptr, events, sizes=(112, 4096), page_elems=128 * 128, reps=10):
+    """Pages between device states and a pinned host pool (the host tier):
+    payload bytes per second over the host link, each direction."""
+    out = {}
+    for n in sizes:
+        perm = torch.from_numpy(np.random.default_rng(8).permutation(n).astype(np.int32)).cuda()
+        states = torch.randn((n, page_elems), device="cuda")
+        pool = torch.empty((n, page_elems), dtype=torch.float32, pin_memory=True)
+        back = torch.empty_like(states)
+        la.la_state_save_host(states, pool, perm)
+        la.la_state_restore_host(pool, perm, back)
+        torch.cuda.synchronize()
+        assert torch.equal(back, states)
+        ms_s = ms_r = 0.0
+        for _ in range(reps):
+            events.record(4, stream_ptr)
+            la.la_state_save_host(states, pool, perm)
+            events.record(5, stream_ptr)
+            la.la_state_restore_host(pool, perm, back)
+            events.record(6, stream_ptr)
+            ms_s += events.ms(4, 5)
+            ms_r += events.ms(5, 6)
+        nbytes = n * page_elems * 4
+        out[f"{n}_pages"] = {"bytes": nbytes, "d2h_GBps": round(nbytes / (ms_s / reps * 1e-3) / 1e9, 1),
+                             "h2d_GBps": round(nbytes / (ms_r / reps * 1e-3) / 1e9, 1),
+                             "d2h_us": round(ms_s / reps * 1e3, 1), "h2d_us": round(ms_r / reps * 1e3, 1)}
+    return out
+
+
 def bench_pool(la, torch, stream_ptr, events, n_pages=4096, page_elems=128 * 128, reps=20):
     """Full-pool scatter and gather under a random permutation (2 x 256 MiB)."""
     rng = np.random.default_rng(7)
@@ -309,6 +340,8 @@ def main():
     if not args.no_pool:
         out["save_restore"] = bench_pool(la, torch, sp, ev)
     out["decode"] = bench_decode(la, torch, sp, ev, H, dk, dv, C)
+    if not args.no_pool:
+        out["host_tier"] = bench_host_tier(la, torch, sp, ev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, B, args.cpu_seconds)
     print(json.dumps(out), flush=True)

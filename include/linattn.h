@@ -204,6 +204,32 @@ la_status la_state_restore_paged(const float *pool, int64_t n_pages,
                                  int64_t n_items, int64_t page_elems,
                                  int32_t *err_count_dev, void *stream);
 
+/*
+ * la_state_save_host / la_state_restore_host - the host-memory tier: the
+ * same page scatter and gather as la_state_save_paged / la_state_restore_paged
+ * with the pool in pinned host memory (the paper's CPU reload path, section
+ * 2.1 and Table 5; section 3.1 requires a save to complete before the pages
+ * are reused, and section 5.5 times CPU reloads).
+ *
+ * host_pool: [n_pages, page_elems] fp32 in pinned host memory mapped into the
+ * device's address space (hipHostMalloc, or a torch tensor allocated with
+ * pin_memory=True), 16-byte aligned; the kernels move pages over the host
+ * link directly.  Both ends of the pool are checked with
+ * hipPointerGetAttributes before any launch: pageable or unmapped memory
+ * returns INVALID_ARG.  states, page ids and err_count are device memory,
+ * with the meanings, -1 / out-of-range handling and alignment of the
+ * device-pool calls.  The copy is asynchronous on `stream`; if done_event
+ * (a hipEvent_t, may be NULL) is given it is recorded after the copy, so the
+ * host may poll or wait on it before reading saved pages (save) or before
+ * overwriting pages being restored (restore).
+ */
+la_status la_state_save_host(const float *states, int64_t n_items, int64_t page_elems,
+                             float *host_pool, int64_t n_pages, const int32_t *page_ids_dev,
+                             int32_t *err_count_dev, void *stream, void *done_event);
+la_status la_state_restore_host(const float *host_pool, int64_t n_pages, const int32_t *page_ids_dev,
+                                float *states, int64_t n_items, int64_t page_elems,
+                                int32_t *err_count_dev, void *stream, void *done_event);
+
 /* Name of a status code (static string). */
 const char *la_status_string(la_status status);
 

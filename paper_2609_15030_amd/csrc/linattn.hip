@@ -366,6 +366,35 @@ la_status decode_dims(const la_shape *s, const la::DecodeArgs &a, hipStream_t st
     return launch_decode<T, 128, 128>(s, a, stream);
 }
 
+// A host-tier pool is pinned host memory mapped into the device's address
+// space (hipHostMalloc, or a torch tensor allocated with pin_memory=True):
+// the copy kernels read or write it directly over the host link.  Both ends
+// of the pool are checked before any launch, so pageable or unmapped memory
+// is rejected instead of being dereferenced by a kernel.  Returns the device
+// address of the pool's first byte.
+la_status host_pool_device_ptr(const float *pool, size_t bytes, float **dev) {
+    *dev = nullptr;
+    if (!pool) return fail(LA_ERR_INVALID_ARG, "host pool is NULL");
+    hipPointerAttribute_t a0{}, a1{};
+    const char *last = (const char *)pool + (bytes ? bytes - 1 : 0);
+    if (hipPointerGetAttributes(&a0, pool) != hipSuccess || hipPointerGetAttributes(&a1, last) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(LA_ERR_INVALID_ARG, "host pool is not pinned, device-mapped host memory");
+    }
+    if (a0.type != hipMemoryTypeHost || a1.type != hipMemoryTypeHost || !a0.devicePointer || !a1.devicePointer)
+        return fail(LA_ERR_INVALID_ARG, "host pool is not pinned, device-mapped host memory");
+    if ((const char *)a1.devicePointer - (const char *)a0.devicePointer != last - (const char *)pool)
+        return fail(LA_ERR_INVALID_ARG, "host pool does not map to one contiguous device range");
+    *dev = (float *)a0.devicePointer;
+    return LA_OK;
+}
+
+la_status record_done(void *done_event, void *stream) {
+    if (done_event && hipEventRecord((hipEvent_t)done_event, (hipStream_t)stream) != hipSuccess)
+        return hip_check("completion event record");
+    return LA_OK;
+}
+
 la_status check_paged(const float *a, const float *b, int64_t n_items, int64_t page_elems, int64_t n_pages,
                       const int32_t *ids) {
     if (n_items < 0 || n_items > 0x7fffffff) return fail(LA_ERR_INVALID_ARG, "n_items=%lld", (long long)n_items);
@@ -456,6 +485,38 @@ la_status la_state_restore_paged(const float *pool, int64_t n_pages, const int32
                        (hipStream_t)stream, (const la::f32x4 *)pool, n_pages, page_ids_dev, (la::f32x4 *)states,
                        page_elems / 4, err_count_dev);
     return hip_check("page restore launch");
+}
+
+la_status la_state_save_host(const float *states, int64_t n_items, int64_t page_elems, float *host_pool,
+                             int64_t n_pages, const int32_t *page_ids_dev, int32_t *err_count_dev, void *stream,
+                             void *done_event) {
+    if (la_status e = check_paged(states, host_pool, n_items, page_elems, n_pages, page_ids_dev)) return e;
+    if (n_items == 0) return record_done(done_event, stream);
+    float *dev = nullptr;
+    if (la_status e = host_pool_device_ptr(host_pool, (size_t)n_pages * page_elems * sizeof(float), &dev)) return e;
+    if (!aligned16(dev)) return fail(LA_ERR_INVALID_ARG, "host pool must be 16-byte aligned");
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(la::page_save_kernel, dim3((unsigned)n_items), dim3(la::kPageThreads), 0,
+                       (hipStream_t)stream, (const la::f32x4 *)states, page_elems / 4, (la::f32x4 *)dev,
+                       n_pages, page_ids_dev, err_count_dev);
+    if (la_status e = hip_check("host-tier save launch")) return e;
+    return record_done(done_event, stream);
+}
+
+la_status la_state_restore_host(const float *host_pool, int64_t n_pages, const int32_t *page_ids_dev, float *states,
+                                int64_t n_items, int64_t page_elems, int32_t *err_count_dev, void *stream,
+                                void *done_event) {
+    if (la_status e = check_paged(states, host_pool, n_items, page_elems, n_pages, page_ids_dev)) return e;
+    if (n_items == 0) return record_done(done_event, stream);
+    float *dev = nullptr;
+    if (la_status e = host_pool_device_ptr(host_pool, (size_t)n_pages * page_elems * sizeof(float), &dev)) return e;
+    if (!aligned16(dev)) return fail(LA_ERR_INVALID_ARG, "host pool must be 16-byte aligned");
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(la::page_restore_kernel, dim3((unsigned)n_items), dim3(la::kPageThreads), 0,
+                       (hipStream_t)stream, (const la::f32x4 *)dev, n_pages, page_ids_dev, (la::f32x4 *)states,
+                       page_elems / 4, err_count_dev);
+    if (la_status e = hip_check("host-tier restore launch")) return e;
+    return record_done(done_event, stream);
 }
 
 const char *la_status_string(la_status status) {

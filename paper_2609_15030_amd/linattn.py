@@ -33,6 +33,7 @@ LA_GDR_DECAYED_DELTA = 1
 
 EXPORTED = ("strict_prefix_boundary", "la_prefill_workspace_bytes", "la_prefill",
             "la_prefill_resume", "la_decode_step", "la_state_save_paged", "la_state_restore_paged",
+            "la_state_save_host", "la_state_restore_host",
             "la_status_string", "la_last_error_message", "la_trace_set_events")
 
 
@@ -75,6 +76,8 @@ def _load() -> ctypes.CDLL:
         "la_decode_step": ([SH, P, P, P, P, P, P, P, P], I32),
         "la_state_save_paged": ([P, I64, I64, P, I64, P, P, P], I32),
         "la_state_restore_paged": ([P, I64, P, P, I64, I64, P, P], I32),
+        "la_state_save_host": ([P, I64, I64, P, I64, P, P, P, P], I32),
+        "la_state_restore_host": ([P, I64, P, P, I64, I64, P, P, P], I32),
         "la_status_string": ([I32], ctypes.c_char_p),
         "la_last_error_message": ([], ctypes.c_char_p),
         "la_trace_set_events": ([ctypes.POINTER(P), I32], None),
@@ -218,6 +221,41 @@ def la_decode_step(shape: LaShape, q, k, v, g, beta, state, o, stream=None, chec
     updated in place, o [n_seqs, H, dv] receives the output."""
     st = _lib.la_decode_step(ctypes.byref(shape), _dptr(q), _dptr(k), _dptr(v), _dptr(g), _dptr(beta),
                              _dptr(state), _dptr(o), _stream(stream))
+    if check:
+        _check(st)
+    return st
+
+
+def _hostptr(t) -> int:
+    """Address of a pinned host tensor (the library checks it is device-mapped)."""
+    if t.is_cuda:
+        raise ValueError("expected a host tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def la_state_save_host(states, host_pool, page_ids_dev, err_count_dev=None, stream=None, done_event=None,
+                       check: bool = True) -> int:
+    """Scatter device states into a pinned host pool ([n_pages, page_elems] fp32)."""
+    n_pages = host_pool.shape[0]
+    page_elems = host_pool[0].numel() if n_pages else states[0].numel()
+    n_items = page_ids_dev.numel()
+    st = _lib.la_state_save_host(_dptr(states), n_items, page_elems, _hostptr(host_pool), n_pages,
+                                 _dptr(page_ids_dev), _dptr(err_count_dev), _stream(stream), done_event)
+    if check:
+        _check(st)
+    return st
+
+
+def la_state_restore_host(host_pool, page_ids_dev, states, err_count_dev=None, stream=None, done_event=None,
+                          check: bool = True) -> int:
+    """Gather pages of a pinned host pool into device states."""
+    n_pages = host_pool.shape[0]
+    page_elems = host_pool[0].numel() if n_pages else states[0].numel()
+    n_items = page_ids_dev.numel()
+    st = _lib.la_state_restore_host(_hostptr(host_pool), n_pages, _dptr(page_ids_dev), _dptr(states), n_items,
+                                    page_elems, _dptr(err_count_dev), _stream(stream), done_event)
     if check:
         _check(st)
     return st
