@@ -190,18 +190,19 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
     __syncthreads();
 
     // ---- 3. A = strictly-lower beta_r exp(Gp_r - G_s) K K^T ------------------
-    // The 10 lower 16x16 tiles are dealt 3/3/2/2 over the waves.  A tile's
-    // row tile is a run-time value, so its gate and beta values are read from
-    // LDS per tile (a register array indexed by it would become a select
-    // chain).
+    // The 10 lower 16x16 tiles (row-major over the lower triangle, diagonal
+    // included) are dealt 3/3/2/2 over the waves.  A tile's row tile is a
+    // run-time value, so its gate and beta values are read from LDS per tile
+    // (a register array indexed by it would become a select chain), and its
+    // coordinates are computed, not looked up (a table indexed at run time
+    // would live in scratch memory).
     {
-        constexpr int tmt[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
-        constexpr int tnt[10] = {0, 0, 1, 0, 1, 2, 0, 1, 2, 3};
 #pragma unroll
         for (int q = 0; q < 3; ++q) {
             const int t = wave + 4 * q;
             if (t < 10) {
-                const int mt = tmt[t], nt = tnt[t];
+                const int mt = t >= 6 ? 3 : t >= 3 ? 2 : t >= 1 ? 1 : 0;
+                const int nt = t - mt * (mt + 1) / 2;
                 const float4 brow = *(const float4 *)&sm.bs[16 * mt + 4 * g16];
                 const float4 gprow = *(const float4 *)&sm.Gp2[16 * mt + 4 * g16];
                 const float gcol = sm.G2[16 * nt + c16];
