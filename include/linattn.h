@@ -157,6 +157,40 @@ la_status la_prefill_resume(const la_shape *shape,
                             void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * la_prefill_stages - run a subset of one prefill call's stages, so that a
+ * caller can overlap them with other work.  The preparation of a resume
+ * depends only on the suffix tokens (section 2.2: the scheduled tokens), so
+ * it can run while the state for prefix [0, B) is still being saved or
+ * restored (section 3.1), and one call's output can run beside the next
+ * call's scan.  `stages` is a mask of
+ *   LA_STAGE_PREPARE (1): chunk-local gate sums and the intra-chunk operands
+ *                         (from k, v, g, beta) into the workspace;
+ *   LA_STAGE_SCAN    (2): the inter-chunk recurrence from state_in (or zero):
+ *                         checkpoints and the final state, plus the per-chunk
+ *                         states the output needs, into the workspace;
+ *   LA_STAGE_OUTPUT  (4): o from q, k and the workspace.
+ * Arguments as la_prefill_resume; start_pos_dev/host NULL make it a cold
+ * call, and then state_in must be NULL.  Every call validates all arguments.
+ * The stages of one call must run in that order on one workspace with the
+ * same arguments; ordering them across streams (events) is the caller's.
+ * la_prefill and la_prefill_resume run all three stages.
+ */
+#define LA_STAGE_PREPARE 1u
+#define LA_STAGE_SCAN 2u
+#define LA_STAGE_OUTPUT 4u
+#define LA_STAGE_ALL 7u
+la_status la_prefill_stages(const la_shape *shape, uint32_t stages,
+                            const void *q, const void *k, const void *v,
+                            const float *g, const float *beta,
+                            const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                            const int64_t *start_pos_dev, const int64_t *start_pos_host,
+                            const float *state_in,
+                            void *o, float *final_state,
+                            float *ckpt_out, const int32_t *ckpt_offsets_dev,
+                            const int32_t *ckpt_offsets_host,
+                            void *workspace, size_t ws_bytes, void *stream);
+
+/*
  * la_decode_step - decode continuation: advance every (sequence, head) by one
  * generated token from its fp32 state (the recurrent state of section 2.1,
  * continued after a cold prefill or a reload; sections 5.1, 5.4 and 5.5

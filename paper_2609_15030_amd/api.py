@@ -109,9 +109,19 @@ class Prefill:
         assert nbytes > 0
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
 
-    def run(self, state_in: Optional[torch.Tensor] = None, stream=None) -> PrefillResult:
+    def run(self, state_in: Optional[torch.Tensor] = None, stream=None, stages: int = la.LA_STAGE_ALL) -> PrefillResult:
+        """All stages (la_prefill / la_prefill_resume), or the subset ``stages``
+        (la_prefill_stages) for callers that overlap stages with other work."""
         x = self.x
         ck = self.ckpt
+        if stages != la.LA_STAGE_ALL:
+            if self.starts is not None:
+                assert state_in is not None
+            la.la_prefill_stages(self.shape, stages, x.q, x.k, x.v, x.g, x.beta, x.cu_dev, x.cu_host,
+                                 self.start_dev, self.starts, state_in if self.starts is not None else None,
+                                 self.o, self.final, ck, self.ckpt_off_dev if ck is not None else None,
+                                 self.ckpt_offsets if ck is not None else None, self.workspace, stream)
+            return PrefillResult(self.o, self.final, ck, self.ckpt_offsets, self.n_ckpt_rows)
         if self.starts is None:
             la.la_prefill(self.shape, x.q, x.k, x.v, x.g, x.beta, x.cu_dev, x.cu_host, self.o,
                           self.final, ck, self.ckpt_off_dev if ck is not None else None,

@@ -151,6 +151,7 @@ struct PrefillCall {
     void *workspace;
     size_t ws_bytes;
     hipStream_t stream;
+    uint32_t stages = LA_STAGE_ALL;
 };
 
 template <typename T, int DK, int DV>
@@ -158,7 +159,7 @@ la_status launch_out(const PrefillCall &c, const la::Workspace &ws, int64_t max_
     const la_shape *s = c.shape;
     const int cps = la::chunks_per_interval(s->ckpt_interval);
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[2], c.stream);
-    if (max_chunks > 0) {
+    if (max_chunks > 0 && (c.stages & LA_STAGE_OUTPUT)) {
         la::OutArgs oa{c.q, c.k, c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
                        (int32_t)max_chunks, s->scale, ws};
         const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
@@ -219,7 +220,7 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[0], c.stream);
     (void)hipGetLastError();
 
-    if (max_chunks > 0) {
+    if (max_chunks > 0 && (c.stages & LA_STAGE_PREPARE)) {
         la::PrepArgs pa{c.k, c.v, c.g, c.beta, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
                         s->variant, (int32_t)max_chunks, ws};
         const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
@@ -227,7 +228,7 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
         if (la_status e = hip_check("chunk preparation launch")) return e;
     }
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[1], c.stream);
-    {
+    if (c.stages & LA_STAGE_SCAN) {
         la::ScanArgs sa{c.cu_dev, c.state_in, c.final_state, c.ckpt_out, c.ckpt_off_dev,
                         s->n_seqs, s->n_heads, s->ckpt_interval, cps, ws, 1, 0, {}};
         constexpr int NT = DV / 16;
@@ -271,6 +272,8 @@ la_status run_prefill(const PrefillCall &c) {
     if (la_status e = check_shape(c.shape)) return e;
     const la_shape *s = c.shape;
     const bool resume = c.start_host != nullptr || c.start_dev != nullptr;
+    if (c.stages == 0 || (c.stages & ~LA_STAGE_ALL)) return fail(LA_ERR_INVALID_ARG, "stages=%u", c.stages);
+    if (!resume && c.state_in) return fail(LA_ERR_INVALID_ARG, "state_in given without start positions");
     const int64_t C = s->ckpt_interval;
     const int cps = la::chunks_per_interval(s->ckpt_interval);
 
@@ -447,6 +450,20 @@ la_status la_prefill_resume(const la_shape *shape, const void *q, const void *k,
     PrefillCall c{shape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host, start_pos_dev, start_pos_host,
                   state_in, o, final_state, ckpt_out, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
                   (hipStream_t)stream};
+    return run_prefill(c);
+}
+
+la_status la_prefill_stages(const la_shape *shape, uint32_t stages, const void *q, const void *k, const void *v,
+                            const float *g, const float *beta, const int32_t *cu_seqlens_dev,
+                            const int32_t *cu_seqlens_host, const int64_t *start_pos_dev,
+                            const int64_t *start_pos_host, const float *state_in, void *o, float *final_state,
+                            float *ckpt_out, const int32_t *ckpt_offsets_dev, const int32_t *ckpt_offsets_host,
+                            void *workspace, size_t ws_bytes, void *stream) {
+    if ((start_pos_dev == nullptr) != (start_pos_host == nullptr))
+        return fail(LA_ERR_INVALID_ARG, "start_pos_dev and start_pos_host go together");
+    PrefillCall c{shape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host, start_pos_dev, start_pos_host,
+                  state_in, o, final_state, ckpt_out, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
+                  (hipStream_t)stream, stages};
     return run_prefill(c);
 }
 

@@ -32,7 +32,7 @@ LA_GDR_LITERAL = 0
 LA_GDR_DECAYED_DELTA = 1
 
 EXPORTED = ("strict_prefix_boundary", "la_prefill_workspace_bytes", "la_prefill",
-            "la_prefill_resume", "la_decode_step", "la_state_save_paged", "la_state_restore_paged",
+            "la_prefill_resume", "la_prefill_stages", "la_decode_step", "la_state_save_paged", "la_state_restore_paged",
             "la_state_save_host", "la_state_restore_host",
             "la_status_string", "la_last_error_message", "la_trace_set_events")
 
@@ -73,6 +73,7 @@ def _load() -> ctypes.CDLL:
         "la_prefill_workspace_bytes": ([SH, I64], SZ),
         "la_prefill": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_prefill_resume": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "la_prefill_stages": ([SH, ctypes.c_uint32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_decode_step": ([SH, P, P, P, P, P, P, P, P], I32),
         "la_state_save_paged": ([P, I64, I64, P, I64, P, P, P], I32),
         "la_state_restore_paged": ([P, I64, P, P, I64, I64, P, P], I32),
@@ -211,6 +212,27 @@ def la_state_restore_paged(pool, page_ids_dev, states, err_count_dev=None, strea
     n_items = page_ids_dev.numel()
     st = _lib.la_state_restore_paged(_dptr(pool), n_pages, _dptr(page_ids_dev), _dptr(states),
                                      n_items, page_elems, _dptr(err_count_dev), _stream(stream))
+    if check:
+        _check(st)
+    return st
+
+
+LA_STAGE_PREPARE, LA_STAGE_SCAN, LA_STAGE_OUTPUT, LA_STAGE_ALL = 1, 2, 4, 7
+
+
+def la_prefill_stages(shape: LaShape, stages: int, q, k, v, g, beta, cu_dev, cu_host, start_dev, start_host,
+                      state_in, o, final_state, ckpt_out, ckpt_off_dev, ckpt_off_host, workspace, stream=None,
+                      check: bool = True) -> int:
+    """A subset of one prefill call's stages (mask of LA_STAGE_*); start_dev /
+    start_host None make it a cold call."""
+    cu_host = np.ascontiguousarray(cu_host, dtype=np.int32)
+    sh = None if start_host is None else np.ascontiguousarray(start_host, dtype=np.int64)
+    oh = None if ckpt_off_host is None else np.ascontiguousarray(ckpt_off_host, dtype=np.int32)
+    st = _lib.la_prefill_stages(ctypes.byref(shape), stages, _dptr(q), _dptr(k), _dptr(v), _dptr(g), _dptr(beta),
+                                _dptr(cu_dev), _hptr(cu_host, np.int32), _dptr(start_dev),
+                                _hptr(sh, np.int64), _dptr(state_in), _dptr(o), _dptr(final_state),
+                                _dptr(ckpt_out), _dptr(ckpt_off_dev), _hptr(oh, np.int32), _dptr(workspace),
+                                workspace.numel() * workspace.element_size(), _stream(stream))
     if check:
         _check(st)
     return st

@@ -133,6 +133,26 @@ def test_paged_validation_before_launch():
     assert lib.la_state_save_paged(FAKE, 0, 8, FAKE, 8, FAKE, None, None) == la.LA_OK   # nothing to do
 
 
+def test_stage_mask_validation_before_launch():
+    lib = la.library()
+    sh = la.make_shape(1, 1, 64, 64, 16)
+    cu = np.array([0, 64], np.int32)
+    P = la.ctypes.c_void_p
+    ws = lib.la_prefill_workspace_bytes(la.ctypes.byref(sh), 64)
+
+    def call(stages, state_in=None, starts=None):
+        st = None if starts is None else np.asarray(starts, np.int64)
+        return lib.la_prefill_stages(la.ctypes.byref(sh), stages, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                     P(cu.ctypes.data), FAKE if st is not None else None,
+                                     P(st.ctypes.data) if st is not None else None, state_in, FAKE, FAKE,
+                                     None, None, None, FAKE, ws, None)
+    assert call(0) == la.LA_ERR_INVALID_ARG
+    assert call(8) == la.LA_ERR_INVALID_ARG
+    assert call(la.LA_STAGE_ALL, state_in=FAKE) == la.LA_ERR_INVALID_ARG      # a state without positions
+    assert call(la.LA_STAGE_PREPARE, starts=[16]) == la.LA_ERR_INVALID_ARG    # resume without a state
+    assert call(la.LA_STAGE_SCAN, state_in=FAKE, starts=[8]) == la.LA_ERR_MISALIGNED_STATE
+
+
 def test_decode_validation_before_launch():
     lib = la.library()
     sh = la.make_shape(2, 8, 128, 128, 256)

@@ -1,0 +1,72 @@
+"""GPU tests of la_prefill_stages: the stages of one prefill call run
+separately, on different streams ordered by events, give the monolithic
+call's results bit for bit.  The resume case prepares its suffix on a side
+stream while the state it starts from is still being restored, the overlap
+the stage split exists for.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_15030_amd import api
+from paper_2609_15030_amd import linattn as la
+from paper_2609_15030_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+P, S, O = la.LA_STAGE_PREPARE, la.LA_STAGE_SCAN, la.LA_STAGE_OUTPUT
+
+
+def _equal(a, b):
+    return (torch.equal(a.o, b.o) and torch.equal(a.final_state, b.final_state)
+            and (a.ckpt is None or torch.equal(a.ckpt, b.ckpt)))
+
+
+@pytest.mark.parametrize("lens,C", [([3584], 256), ([4096, 1500], 1024), ([1000, 3584, 257], 256)])
+def test_cold_stages_across_streams_equal_monolithic(lens, C):
+    x = wl.random_inputs(60 + C, lens, 8, 128, 128, gate_scale=0.01)
+    xd = api.to_device(x)
+    ref = api.Prefill(xd, C).run()
+    p = api.Prefill(xd, C)
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    p.run(stream=main, stages=P | S)
+    done_scan = torch.cuda.Event()
+    done_scan.record(main)
+    side.wait_event(done_scan)
+    with torch.cuda.stream(side):
+        p.run(stream=side, stages=O)
+    main.wait_stream(side)
+    torch.cuda.synchronize()
+    res = api.PrefillResult(p.o, p.final, p.ckpt, p.ckpt_offsets, p.n_ckpt_rows)
+    torch.cuda.synchronize()
+    assert _equal(res, ref)
+
+
+@pytest.mark.parametrize("C", [256, 1024])
+def test_resume_prepared_while_state_restores(C):
+    N, H = 4096, 8
+    x = wl.random_inputs(70 + C, [N], H, 128, 128, gate_scale=0.01)
+    cold = api.prefill(api.to_device(x), C)
+    B = la.strict_prefix_boundary(N, C, N)
+    j = B // C - 1
+    n_ck = cold.n_ckpt_rows
+    pool = torch.empty((n_ck * H, 128 * 128), device="cuda")
+    ids = torch.arange(n_ck * H, dtype=torch.int32, device="cuda")
+    la.la_state_save_paged(cold.ckpt, pool, ids)
+    torch.cuda.synchronize()
+    xs = api.to_device(x.tokens(B, N))
+    ref = api.prefill_resume(xs, [B], cold.ckpt[j:j + 1].clone(), C)
+    # restore on the main stream while the suffix is prepared on a side stream
+    state = torch.full((1, H, 128, 128), float("nan"), device="cuda")
+    r = api.Prefill(xs, C, starts=[B])
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    side.wait_stream(main)                 # the suffix inputs were copied on main
+    with torch.cuda.stream(side):
+        r.run(state, stream=side, stages=P)
+    la.la_state_restore_paged(pool, ids[j * H:(j + 1) * H].contiguous(), state, stream=main)
+    main.wait_stream(side)
+    r.run(state, stream=main, stages=S | O)
+    torch.cuda.synchronize()
+    assert torch.equal(r.o, ref.o) and torch.equal(r.final, ref.final_state) and torch.equal(r.ckpt, ref.ckpt)
+    assert torch.equal(r.o, cold.o[B:]) and torch.equal(r.final, cold.final_state)
