@@ -76,25 +76,30 @@ class HipEvents:
 def flops_per_token_head(dk, dv, L=CHUNK):
     """Algorithmic flops per (token, head), triangular products counted once.
 
-    prep:  K K^T (L dk), W = X (..K) (L dk), U~ = X (..V) (L dv), inverse (L^2 / 3)
+    prep:  K K^T (L dk), W = X (..K) (L dk), U~ = X (..V) (L dv), inverse (L^2 / 3),
+           Q K^T (L dk)
     scan:  W S (2 dk dv), K~^T U (2 dk dv)
-    out:   Q S (2 dk dv), Q K^T (L dk), P U (L dv)
+    out:   Q S (2 dk dv), P U (L dv)
     """
-    return {"prep": 2 * L * dk + L * dv + L * L / 3,
+    return {"prep": 3 * L * dk + L * dv + L * L / 3,
             "scan": 4 * dk * dv,
-            "out": 2 * dk * dv + L * dk + L * dv}
+            "out": 2 * dk * dv + L * dv}
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "prefill_tp_rank_T3584_hbm_counters.md")
 SCAN_SOURCES = ["paper_2609_15030_amd/csrc/la_common.h", "paper_2609_15030_amd/csrc/gdr_scan.h",
+                "paper_2609_15030_amd/csrc/gdr_out.h",
                 "paper_2609_15030_amd/csrc/linattn.hip", "paper_2609_15030_amd/build.py"]
 
 
 def scan_kernel_name(io_bf16, dk):
-    """The scan form the library launches (its default choice, or LA_SCAN_WAVES)."""
+    """The scan form the library launches for the benchmark's single-level
+    interval (its default choice, or LA_SCAN_WAVES / LA_SCAN_OUTPUT)."""
     forced = os.environ.get("LA_SCAN_WAVES", "")
     waves = int(forced) if forced in ("1", "4") else (4 if (not io_bf16 and dk == 128) else 1)
-    return "gdr_scan1_kernel" if waves == 1 else "gdr_scan_kernel"
+    if waves != 1:
+        return "gdr_scan_kernel"
+    return "gdr_scan1_kernel" if os.environ.get("LA_SCAN_OUTPUT", "") == "0" else "gdr_scan1o_kernel"
 
 
 def measured_traffic(kernel):
@@ -310,15 +315,21 @@ def main():
         stage["out"] += ev.ms(2, 3)
     stage_us = {k: v / n_trace * 1e3 for k, v in stage.items()}
     fl = flops_per_token_head(dk, dv)
-    dom = max(stage_us, key=stage_us.get)
-    achieved = fl[dom] * N * H / (stage_us[dom] * 1e-6) / 1e12
+    scan_name = scan_kernel_name(True, dk)
+    fused = scan_name == "gdr_scan1o_kernel"
+    # with the scan's output wave the output product runs inside the scan
+    # kernel (no output launch: the "out" interval is the gap between two
+    # events with no kernel between them)
+    kfl = dict(fl, scan=fl["scan"] + fl["out"], out=0.0) if fused else fl
+    dom = max(("prep", "scan", "out"), key=stage_us.get)
+    achieved = kfl[dom] * N * H / (stage_us[dom] * 1e-6) / 1e12
     prefill_us = sum(stage_us.values())
-    kname = {"prep": "gdr_prep_kernel", "scan": scan_kernel_name(True, dk), "out": "gdr_out_kernel"}[dom]
+    kname = {"prep": "gdr_prep_kernel", "scan": scan_name, "out": "gdr_out_kernel"}[dom]
     roofline = {"bound": "mfma", "kernel": kname,
                 "achieved": round(achieved, 3), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_PEAK_TFLOPS, 5), "traffic": measured_traffic(kname),
                 "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)",
-                "flops_per_launch": fl[dom] * N * H, "avg_launch_us": round(stage_us[dom], 2)}
+                "flops_per_launch": kfl[dom] * N * H, "avg_launch_us": round(stage_us[dom], 2)}
 
     out = {
         "metric": "linear-attn prefill tokens/s per rank + % MFMA peak; state save/restore GB/s",
@@ -334,6 +345,7 @@ def main():
         "gpu_ms_per_step": round(gpu_ms / args.steps, 4),
         "cold_prefill": {"us": round(prefill_us, 2), "tokens_per_s": round(N / (prefill_us * 1e-6), 1),
                          "stage_us": {k: round(v, 2) for k, v in stage_us.items()},
+                         "scan_kernel": scan_name, "output_in_scan": fused,
                          "alg_tflops": round(sum(fl.values()) * N * H / (prefill_us * 1e-6) / 1e12, 3)},
         "roofline": roofline,
     }

@@ -1,9 +1,23 @@
-// Output read-out: parallel over (chunk, head, sequence), 4 waves each.
-// For chunk rows r, with S_0 the state entering the chunk and U from the
-// scan:
-//   o_r = scale * ( exp(G_r) (S_0^T q_r) + sum_{s<=r} exp(G_r - G_s) (q_r . k_s) u_s )
-// i.e. O = scale * ( diag(exp G) Q S_0 + (Q K^T  masked r>=s, decayed) U ),
-// the read-out of the post-update state S_r^T q_r.
+// Output read-out of a chunk, one 16-column tile of the state at a time.
+//
+// For chunk rows r (tokens) and s, with S_0 the state entering the chunk, U
+// the chunk's corrections (U = U~ - W S_0) and
+//   P_rs = (q_r . k_s) exp(G_r - G_s) for s <= r, zero above the diagonal
+// (written by the preparation kernel), the read-out of the post-update
+// state S_r^T q_r is
+//   o_r = scale * ( exp(G_r) S_0^T q_r + sum_s P_rs u_s ).
+// Per 16-token tile it is computed transposed,
+//   O^T = scale * ( (S_0^T Q^T) diag(exp G) + U^T P^T ),
+// because then the state and U enter as A operands straight from the scan's
+// registers (per lane, the A operand of X^T holds the same values as the B
+// operand of X, including the contraction-index permutation perm_row), Q^T
+// and P^T are B operands (both written by the preparation kernel in that
+// order, read here with whole 16-byte vectors), and each lane ends with 4
+// consecutive output columns of one token: one 8-byte (bf16) or 16-byte
+// (fp32) store.
+//
+// The scan kernel's output wave and the split output kernel run this same
+// code on the same operands, so both paths produce identical bits.
 #pragma once
 #include "la_common.h"
 
@@ -11,8 +25,90 @@ namespace la {
 
 constexpr float kLog2eOut = 1.4426950408889634f;
 
+// One chunk's read-out operands that every column tile shares, as one lane
+// holds them (g = lane / 16, c = lane % 16):
+//   q[mt][f] = Q[16 mt + c][perm_row(f, g)]      (B operand of Q^T, dk permuted)
+//   p[mt][f] = P[16 mt + c][perm_row(f, g)]      (B operand of P^T, chunk rows permuted)
+//   eg[mt]   = exp(G_{16 mt + c})
+template <typename T, int DK> struct OutFrag {
+    static constexpr int FS = DK / 4, FU = kChunk / 4;
+    T q[4][FS];
+    T p[4][FU];
+    float eg[4];
+};
+
+template <typename T> __device__ inline void buf_store_4(__amdgpu_buffer_rsrc_t r, uint32_t voff, const T *src);
+template <> __device__ inline void buf_store_4<__bf16>(__amdgpu_buffer_rsrc_t r, uint32_t voff, const __bf16 *src) {
+    buf_store8(*(const uint2 *)src, r, voff, 0u);
+}
+template <> __device__ inline void buf_store_4<float>(__amdgpu_buffer_rsrc_t r, uint32_t voff, const float *src) {
+    buf_store16(*(const uint4 *)src, r, voff, 0u);
+}
+
+// Byte range of rows [0, n) of one head in a [tokens, H, D] tensor, counted
+// from row 0 of that head: row n and later fall outside it, so buffer
+// accesses to them read zero and drop stores (the chunk's ragged tail).
+// The value is wave-uniform; readfirstlane keeps it in a scalar register
+// (a buffer resource held in vector registers costs a loop per access).
+template <typename T> __device__ inline uint32_t head_rows_bytes(int n, int H, int D) {
+    const uint32_t b = ((uint32_t)(n - 1) * (uint32_t)H * (uint32_t)D + (uint32_t)D) * (uint32_t)sizeof(T);
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)b);
+}
+
+// Issues the loads of one chunk's read-out operands: the Q and P fragments
+// and the gates of workspace slot-head sh.
+template <typename T, int DK>
+__device__ inline void load_out_frag(OutFrag<T, DK> &f, const Workspace &ws, int64_t sh) {
+    constexpr int VEC = Vec<T>::N, VS = OutFrag<T, DK>::FS / VEC, VU = OutFrag<T, DK>::FU / VEC;
+    const int lane = threadIdx.x & 63, c16 = lane & 15;
+    constexpr size_t QE = (size_t)kChunk * DK;       // Q elements per slot-head
+    const auto rq = make_rsrc((const T *)ws.qf + sh * QE, QE * sizeof(T));
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int v = 0; v < VS; ++v)
+            *(uint4 *)&f.q[mt][v * VEC] = buf_load16(rq, 16u * (uint32_t)lane, 1024u * (mt * VS + v));
+    constexpr size_t PE = (size_t)kChunk * kChunk;   // P elements per slot-head
+    const auto rp = make_rsrc((const T *)ws.p + sh * PE, PE * sizeof(T));
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int v = 0; v < VU; ++v)
+            *(uint4 *)&f.p[mt][v * VEC] = buf_load16(rp, 16u * (uint32_t)lane, 1024u * (mt * VU + v));
+    const auto rg = make_rsrc(ws.g + sh * kChunk, kChunk * sizeof(float));
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) f.eg[mt] = buf_load4f(rg, 4u * (uint32_t)(16 * mt + c16), 0u);
+}
+
+// O^T for one 16-column tile of the state: sb and ub are the scan's operand
+// forms of S_0 (B-operand order of S_0, i.e. A-operand order of S_0^T) and
+// of U; o is the output of head h at chunk row 0, rows n and later masked.
+template <typename T, int DK>
+__device__ inline void out_tile(const OutFrag<T, DK> &f, const T *sb, const T *ub, float scale, T *o, int n,
+                                int H, int DV, int tile) {
+    using M = MT<T>;
+    constexpr int KW = M::KW, FS = OutFrag<T, DK>::FS, FU = OutFrag<T, DK>::FU;
+    const int lane = threadIdx.x & 63, g16 = lane >> 4, c16 = lane & 15;
+    const auto ro = make_rsrc(o, head_rows_bytes<T>(n, H, DV));
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int ks = 0; ks < FS / KW; ++ks) acc = M::mma(M::pack(&sb[ks * KW]), M::pack(&f.q[mt][ks * KW]), acc);
+        const float eg = __builtin_amdgcn_exp2f(f.eg[mt] * kLog2eOut);
+        acc = acc * eg;
+#pragma unroll
+        for (int ks = 0; ks < FU / KW; ++ks) acc = M::mma(M::pack(&ub[ks * KW]), M::pack(&f.p[mt][ks * KW]), acc);
+        T out[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) out[i] = from_f32<T>(acc[i] * scale);
+        const uint32_t voff = ((uint32_t)(16 * mt + c16) * (uint32_t)(H * DV) + (uint32_t)(16 * tile + 4 * g16)) *
+                              (uint32_t)sizeof(T);
+        buf_store_4<T>(ro, voff, out);
+    }
+}
+
 struct OutArgs {
-    const void *q, *k;
     void *o;
     const int32_t *cu;
     int32_t n_seqs, n_heads, C, cps, max_chunks;
@@ -20,27 +116,17 @@ struct OutArgs {
     Workspace ws;
 };
 
-template <typename T, int DK, int DV> struct alignas(16) OutSmem {
-    static constexpr int PK = Vec<T>::N;
-    T qs[kChunk][DK + PK];
-    T ks[kChunk][DK + PK];
-    T ps[kChunk][kChunk + PK];        // decayed, masked Q K^T
-    T os[kChunk][DV + PK];            // output staging for coalesced stores
-    float G[kChunk];                  // log2(e)-scaled cumulative gate
-};
-
+// Split output kernel (used when the scan ran without its output wave: the
+// two-level scan, the dk-split scan, and a call that runs the output stage
+// on its own): one workgroup per (chunk, head, sequence), one wave per
+// column tile, reading the state entering the chunk and U from the
+// workspace.
 template <typename T, int DK, int DV>
-__global__ __launch_bounds__(256, 2) void gdr_out_kernel(OutArgs a) {
-    using M = MT<T>;
+__global__ __launch_bounds__(4 * DV) void gdr_out_kernel(OutArgs a) {
     using L = WsLayout<T, DK, DV>;
-    constexpr int KW = M::KW, KSTEP = M::KSTEP, VEC = Vec<T>::N;
-    constexpr int FS = DK / 4, FU = kChunk / 4;
-    constexpr int NTW = DV / 16 / 4;  // output column tiles per wave
-    static_assert(NTW >= 1, "dv >= 64");
-    __shared__ OutSmem<T, DK, DV> sm;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int g16 = lane >> 4, c16 = lane & 15;
+    constexpr int VEC = Vec<T>::N, FS = DK / 4, FU = kChunk / 4;
+    constexpr int VS = FS / VEC, VU = FU / VEC;
+    const int lane = threadIdx.x & 63, tile = threadIdx.x >> 6;
     int64_t j;
     int seq, h;
     if (!unit_of_block(a.n_seqs, a.n_heads, a.max_chunks, &seq, &h, &j)) return;
@@ -54,122 +140,16 @@ __global__ __launch_bounds__(256, 2) void gdr_out_kernel(OutArgs a) {
     const int64_t t0 = cu0 + lo;
     const int64_t sh = (slot_base(cu0, seq, a.C, a.cps) + j) * H + h;
 
-    // state entering the chunk and U for this wave's column tiles (issued
-    // first, so their latency overlaps the Q and K staging loads)
-    T sc[NTW][FS], ub[NTW][FU];
-    {
-        const T *scsrc = (const T *)a.ws.sc + sh * L::sc_elems;
-        const T *usrc = (const T *)a.ws.u + sh * L::u_elems;
+    T sb[FS], ub[FU];
+    const auto rs = make_rsrc((const T *)a.ws.sc + sh * L::sc_elems, L::sc_elems * sizeof(T));
+    const auto ru = make_rsrc((const T *)a.ws.u + sh * L::u_elems, L::u_elems * sizeof(T));
 #pragma unroll
-        for (int w = 0; w < NTW; ++w) {
-            const int nt = wave * NTW + w;
+    for (int v = 0; v < VS; ++v) *(uint4 *)&sb[v * VEC] = buf_load16(rs, 16u * lane, 1024u * (tile * VS + v));
 #pragma unroll
-            for (int v = 0; v < FS / VEC; ++v)
-                *(uint4 *)&sc[w][v * VEC] = ((const uint4 *)scsrc)[(nt * (FS / VEC) + v) * 64 + lane];
-#pragma unroll
-            for (int v = 0; v < FU / VEC; ++v)
-                *(uint4 *)&ub[w][v * VEC] = ((const uint4 *)usrc)[(nt * (FU / VEC) + v) * 64 + lane];
-        }
-    }
-    const T *qin = (const T *)a.q;
-    const T *kin = (const T *)a.k;
-    {
-        // all loads in flight before the first LDS store; rows past the end
-        // read the last valid row and are zeroed
-        constexpr int IT = kChunk * DK / VEC / 256;
-        static_assert(IT * 256 * VEC == kChunk * DK, "tiling");
-        uint4 qv[IT], kv[IT];
-#pragma unroll
-        for (int it = 0; it < IT; ++it) {
-            const int vi = tid + 256 * it, r = vi / (DK / VEC), c = (vi % (DK / VEC)) * VEC;
-            const int rr = r < n ? r : n - 1;
-            qv[it] = *(const uint4 *)(qin + ((t0 + rr) * H + h) * DK + c);
-            kv[it] = *(const uint4 *)(kin + ((t0 + rr) * H + h) * DK + c);
-        }
-        const float gl = tid < kChunk ? a.ws.g[sh * kChunk + tid] : 0.f;
-#pragma unroll
-        for (int it = 0; it < IT; ++it) {
-            const int vi = tid + 256 * it, r = vi / (DK / VEC), c = (vi % (DK / VEC)) * VEC;
-            if (r >= n) {
-                qv[it] = make_uint4(0, 0, 0, 0);
-                kv[it] = make_uint4(0, 0, 0, 0);
-            }
-            *(uint4 *)&sm.qs[r][c] = qv[it];
-            *(uint4 *)&sm.ks[r][c] = kv[it];
-        }
-        if (tid < kChunk) sm.G[tid] = gl * kLog2eOut;
-    }
-    __syncthreads();
-
-    // log2(e)-scaled cumulative gates this lane needs, read once
-    float grow[4][4], gcol[4];
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) grow[mt][i] = sm.G[16 * mt + 4 * g16 + i];
-        gcol[mt] = sm.G[16 * mt + c16];
-    }
-
-    // P = (Q K^T) * exp(G_r - G_s) on r >= s, zero above the diagonal
-    {
-        const int mt = wave;     // run-time row tile: its gates come from LDS
-        const float4 gw4 = *(const float4 *)&sm.G[16 * mt + 4 * g16];
-        const float gw[4] = {gw4.x, gw4.y, gw4.z, gw4.w};
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-            f32x4 acc = zero4();
-            if (nt <= mt) {
-#pragma unroll
-                for (int ks = 0; ks < DK / KSTEP; ++ks)
-                    acc = M::mma(M::pack(&sm.qs[16 * mt + c16][ks * KSTEP + g16 * KW]),
-                                 M::pack(&sm.ks[16 * nt + c16][ks * KSTEP + g16 * KW]), acc);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = 16 * mt + 4 * g16 + i, s = 16 * nt + c16;
-                const float e = __builtin_amdgcn_exp2f(gw[i] - gcol[nt]);
-                sm.ps[r][s] = from_f32<T>((s <= r) ? acc[i] * e : 0.f);
-            }
-        }
-    }
-    __syncthreads();
-
-#pragma unroll
-    for (int w = 0; w < NTW; ++w) {
-        const int nt = wave * NTW + w;
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            const int r = 16 * mt + c16;
-            f32x4 acc = zero4();
-            // Q S_0 (contraction over dk in the state's permuted order)
-#pragma unroll
-            for (int ks = 0; ks < FS / KW; ++ks) {
-                const int f0 = ks * KW;
-                const typename M::frag fa =
-                    M::pack2(&sm.qs[r][perm_row(f0, g16)], &sm.qs[r][perm_row(f0 + (KW > 4 ? 4 : 0), g16)]);
-                acc = M::mma(fa, M::pack(&sc[w][f0]), acc);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) acc[i] *= __builtin_amdgcn_exp2f(grow[mt][i]);
-            // + P U (contraction over chunk rows in U's permuted order)
-#pragma unroll
-            for (int ks = 0; ks < FU / KW; ++ks) {
-                const int f0 = ks * KW;
-                const typename M::frag fa =
-                    M::pack2(&sm.ps[r][perm_row(f0, g16)], &sm.ps[r][perm_row(f0 + (KW > 4 ? 4 : 0), g16)]);
-                acc = M::mma(fa, M::pack(&ub[w][f0]), acc);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                sm.os[16 * mt + 4 * g16 + i][16 * nt + c16] = from_f32<T>(acc[i] * a.scale);
-        }
-    }
-    __syncthreads();
-    T *oout = (T *)a.o;
-    for (int vi = tid; vi < kChunk * DV / VEC; vi += 256) {
-        const int r = vi / (DV / VEC), c = (vi % (DV / VEC)) * VEC;
-        if (r < n) *(uint4 *)(oout + ((t0 + r) * H + h) * DV + c) = *(const uint4 *)&sm.os[r][c];
-    }
+    for (int v = 0; v < VU; ++v) *(uint4 *)&ub[v * VEC] = buf_load16(ru, 16u * lane, 1024u * (tile * VU + v));
+    OutFrag<T, DK> f;
+    load_out_frag<T, DK>(f, a.ws, sh);
+    out_tile<T, DK>(f, sb, ub, a.scale, (T *)a.o + (t0 * H + h) * DV, n, H, DV, tile);
 }
 
 }  // namespace la

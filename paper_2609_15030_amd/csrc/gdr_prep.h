@@ -10,6 +10,9 @@
 //   W     = X diag(beta exp(Gp)) K             (stored negated, A-operand order)
 //   U~    = X diag(beta) V                     (fp32, C-layout)
 //   K~^T  = (diag(exp(G_63 - G)) K)^T          (A-operand order, chunk rows permuted)
+//   P     = (Q K^T) exp(G_r - G_s) on s <= r   (for the output; B operand of P^T
+//                                               per token tile, chunk rows permuted)
+//   Q     = the queries as the B operand of Q^T per token tile (dk permuted)
 // so that, for the state S_0 entering the chunk, U = U~ - W S_0 holds the
 // per-row corrections u_r = beta_r (v_r - pred_r) and the state leaving the
 // chunk is exp(G_63) S_0 + K~^T U.  (Derivation: unroll the recurrence
@@ -26,7 +29,7 @@
 namespace la {
 
 struct PrepArgs {
-    const void *k, *v;
+    const void *q, *k, *v;
     const float *g, *beta;
     const int32_t *cu;
     int32_t n_seqs, n_heads, C, cps, variant, max_chunks;
@@ -128,6 +131,24 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
 
     const T *kin = (const T *)a.k;
     const T *vin = (const T *)a.v;
+
+    // This lane's queries: token row 16 wave + lane % 16 at dk perm_row(f, g)
+    // for f < DK/4 (g = lane / 16), runs of 4.  That is exactly this lane's
+    // part of the B operand of Q^T for token tile `wave` in the order the
+    // state's accumulator layout contracts dk, so it is stored as is for the
+    // output, and the P product below contracts dk in the same order.
+    T qf[DK / 4];
+    {
+        const int r = 16 * wave + c16, rr = r < n ? r : n - 1;
+        const T *qrow = (const T *)a.q + ((t0 + rr) * H + h) * DK + 4 * g16;
+#pragma unroll
+        for (int p4 = 0; p4 < DK / 16; ++p4) {
+            if constexpr (sizeof(T) == 2)
+                *(uint2 *)&qf[4 * p4] = *(const uint2 *)(qrow + 16 * p4);
+            else
+                *(uint4 *)&qf[4 * p4] = *(const uint4 *)(qrow + 16 * p4);
+        }
+    }
 
     // ---- 1. stage K, V (row-major), g, beta; clear X ------------------------
     // Every global load is issued before the first use; rows past the
@@ -329,6 +350,45 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
 #pragma unroll
             for (int v = 0; v < NV2; ++v)
                 *(uint4 *)(kout + ((size_t)(kt * NV2 + v) * 64 + lane) * VEC) = *(const uint4 *)&vals[v * VEC];
+        }
+        // P for token tile mt, computed as the tiles K Q^T: the result tile
+        // (s tile nt, token tile mt) holds P[16 mt + c16][16 nt + 4 g + i] in
+        // lane (g, c16), which is element 4 nt + i of that lane's P^T
+        // operand, so the fragments are stored straight from the
+        // accumulators.  Tiles above the diagonal are zero.
+        {
+            const float gr = sm.G2[16 * mt + c16];
+            T vals[16];
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+                f32x4 acc = zero4();
+                if (nt <= mt) {
+#pragma unroll
+                    for (int ks = 0; ks < DK / KSTEP; ++ks) {
+                        const int f0 = ks * KW;
+                        const T *krow = &sm.ks[16 * nt + c16][0];
+                        acc = M::mma(M::pack2(krow + perm_row(f0, g16), krow + perm_row(f0 + (KW > 4 ? 4 : 0), g16)),
+                                     M::pack(&qf[f0]), acc);
+                    }
+                }
+                const float4 gs = *(const float4 *)&sm.G2[16 * nt + 4 * g16];
+                const float gsv[4] = {gs.x, gs.y, gs.z, gs.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int s = 16 * nt + 4 * g16 + i, r = 16 * mt + c16;
+                    const float e = __builtin_amdgcn_exp2f(gr - gsv[i]);
+                    vals[4 * nt + i] = from_f32<T>(s <= r ? acc[i] * e : 0.f);
+                }
+            }
+            T *pout = (T *)a.ws.p + sh * WsLayout<T, DK, DV>::p_elems;
+#pragma unroll
+            for (int v = 0; v < NV2; ++v)
+                *(uint4 *)(pout + ((size_t)(mt * NV2 + v) * 64 + lane) * VEC) = *(const uint4 *)&vals[v * VEC];
+            constexpr int NQ = DK / 4 / VEC;
+            T *qout = (T *)a.ws.qf + sh * WsLayout<T, DK, DV>::qf_elems;
+#pragma unroll
+            for (int v = 0; v < NQ; ++v)
+                *(uint4 *)(qout + ((size_t)(mt * NQ + v) * 64 + lane) * VEC) = *(const uint4 *)&qf[v * VEC];
         }
     }
     __syncthreads();   // every wave is done reading ks and vs

@@ -22,6 +22,7 @@
 // U (io type), and writes fp32 checkpoints and the final state.
 #pragma once
 #include "la_common.h"
+#include "gdr_out.h"
 
 namespace la {
 
@@ -48,6 +49,8 @@ struct ScanArgs {
     Workspace ws;
     int32_t seg_m, max_seg;       // two-level scan only
     SegWorkspace seg;
+    void *o;                      // scan with output wave only: output [T, H, dv] (io type)
+    float scale;
 };
 
 // Chunk bounds of one sequence, advanced by additions only (the plan of
@@ -329,16 +332,34 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
 }
 
 
+// Operand forms of the state entering a chunk and of U, handed from the scan
+// wave to the output wave of the same workgroup through LDS: two slots
+// (chunk parity), each lane's values as 16-byte vectors [vector][lane].
+template <typename T, int DK> struct Handoff {
+    static constexpr int VS = DK / 4 / Vec<T>::N, VU = kChunk / 4 / Vec<T>::N;
+    uint4 sb[2][VS][64];
+    uint4 ub[2][VU][64];
+};
+
+// Workgroup barrier that orders LDS only: the release fence waits for this
+// wave's LDS accesses (not for its global loads in flight).
+__device__ inline void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
 // Single-wave form.  One wave owns a 16-column tile of the state and all DK
 // rows, kept in fp32 MFMA result registers, so a chunk needs no workgroup
 // synchronisation: 4 * DK/32 MFMAs for U = U~ - W S and 2 * DK/16 for the
 // state update, with the next chunk's operands in flight while one is
 // computed.  scan1_chunks runs the whole sequence of one (sequence, head) on
-// one tile: it hands the output kernel the state entering each chunk and U,
-// and writes the checkpoints.
+// one tile and writes the checkpoints.  It hands the state entering each
+// chunk and U to the split output kernel through the workspace or, with hs
+// set, to the workgroup's output wave through LDS (one barrier per chunk).
 template <typename T, int DK, int DV>
 __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile, int len, int64_t base,
-                                    int nch, f32x4 (&S)[DK / 16]) {
+                                    int nch, f32x4 (&S)[DK / 16], Handoff<T, DK> *hs = nullptr) {
     using M = MT<T>;
     using L = WsLayout<T, DK, DV>;
     constexpr int KW = M::KW, VEC = Vec<T>::N;
@@ -391,7 +412,10 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
         T sb[FS];
 #pragma unroll
         for (int f = 0; f < FS; ++f) sb[f] = from_f32<T>(S[f >> 2][f & 3]);
-        {
+        if (hs) {
+#pragma unroll
+            for (int v = 0; v < VS; ++v) hs->sb[jj & 1][v][lane] = *(const uint4 *)&sb[v * VEC];
+        } else {
             const auto rs = make_rsrc((T *)a.ws.sc + sh * L::sc_elems, L::sc_elems * sizeof(T));
 #pragma unroll
             for (int v = 0; v < VS; ++v)
@@ -410,7 +434,10 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
         T ub[FU];
 #pragma unroll
         for (int f = 0; f < FU; ++f) ub[f] = from_f32<T>(U[f >> 2][f & 3]);
-        {
+        if (hs) {
+#pragma unroll
+            for (int v = 0; v < VU; ++v) hs->ub[jj & 1][v][lane] = *(const uint4 *)&ub[v * VEC];
+        } else {
             const auto rs = make_rsrc((T *)a.ws.u + sh * L::u_elems, L::u_elems * sizeof(T));
 #pragma unroll
             for (int v = 0; v < VU; ++v)
@@ -441,8 +468,38 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
             const int row = ckpt_row++;
             if (a.ckpt) store_state_tiles<RT, DV>(a.ckpt + ((size_t)row * H + h) * DK * DV, S, lane_off);
         }
+        if (hs) lds_barrier();   // this chunk's slot is written; the output wave may read it
     };
     scan_ring<1>(nch, load, step, (Ops *)nullptr);
+}
+
+// The output wave of the scan-with-output kernel: per chunk, waits for the
+// scan wave's handoff of that chunk, then computes and stores the chunk's
+// output for the tile (out_tile).  Its own operands (Q and P fragments, gates) are
+// loaded one chunk ahead.  It passes exactly one barrier per chunk, as the
+// scan wave does; reading slot j & 1 before the barrier of chunk j + 1 keeps
+// the scan wave from overwriting it (that write follows that barrier).
+template <typename T, int DK, int DV>
+__device__ inline void out_wave_chunks(const ScanArgs &a, int h, int tile, int64_t cu0, int len, int64_t base,
+                                       int nch, const Handoff<T, DK> *hs) {
+    using F = OutFrag<T, DK>;
+    constexpr int VEC = Vec<T>::N, VS = Handoff<T, DK>::VS, VU = Handoff<T, DK>::VU;
+    const int lane = threadIdx.x & 63, H = a.n_heads;
+    ChunkCursor cur{0, a.C, len, a.C};
+    auto load = [&](F &f, int jj) { load_out_frag<T, DK>(f, a.ws, (base + jj) * H + h); };
+    auto step = [&](const F &f, int jj) {
+        const int lo = cur.pos;
+        cur.advance();
+        const int n = cur.pos - lo;
+        lds_barrier();
+        T sb[VS * VEC], ub[VU * VEC];
+#pragma unroll
+        for (int v = 0; v < VS; ++v) *(uint4 *)&sb[v * VEC] = hs->sb[jj & 1][v][lane];
+#pragma unroll
+        for (int v = 0; v < VU; ++v) *(uint4 *)&ub[v * VEC] = hs->ub[jj & 1][v][lane];
+        out_tile<T, DK>(f, sb, ub, a.scale, (T *)a.o + ((cu0 + lo) * H + h) * DV, n, H, DV, tile);
+    };
+    scan_ring<1>(nch, load, step, (F *)nullptr);
 }
 
 // Loads a [DK][DV] fp32 state's tile into C layout (or zeros for null).
@@ -482,6 +539,39 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
         const int lane = threadIdx.x;
         store_state_tiles<DK / 16, DV>(a.final_state + state_off, S,
                                        4u * (uint32_t)(4 * (lane >> 4) * DV + 16 * tile + (lane & 15)));
+    }
+}
+
+// Scan with output: the single-wave scan of gdr_scan1_kernel (wave 0) plus
+// an output wave (wave 1) per (sequence, head, 16-column tile).  The state
+// entering each chunk and U go from one wave to the other through LDS, so
+// they never reach HBM, and the output product runs on another SIMD beside
+// the scan's chain.
+template <typename T, int DK, int DV>
+__global__ __launch_bounds__(128) void gdr_scan1o_kernel(ScanArgs a) {
+    constexpr int NT = DV / 16;
+    __shared__ Handoff<T, DK> hs;
+    const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
+    const int pair = xcd + 8 * (q / NT), tile = q % NT;
+    const int H = a.n_heads;
+    if (pair >= a.n_seqs * H) return;
+    const int seq = pair / H, h = pair % H;
+    const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
+    const int nch = n_chunks32(len, a.C, a.cps);
+    const int64_t base = slot_base(cu0, seq, a.C, a.cps);
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    if (wave == 0) {
+        const size_t state_off = (size_t)pair * DK * DV;
+        f32x4 S[DK / 16];
+        load_state_tile<DK, DV>(a.state_in ? a.state_in + state_off : nullptr, tile, S);
+        scan1_chunks<T, DK, DV>(a, seq, h, tile, len, base, nch, S, &hs);
+        if (a.final_state) {
+            const int lane = threadIdx.x & 63;
+            store_state_tiles<DK / 16, DV>(a.final_state + state_off, S,
+                                           4u * (uint32_t)(4 * (lane >> 4) * DV + 16 * tile + (lane & 15)));
+        }
+    } else {
+        out_wave_chunks<T, DK, DV>(a, h, tile, cu0, len, base, nch, &hs);
     }
 }
 

@@ -73,6 +73,18 @@ __device__ inline void buf_store16(uint4 x, __amdgpu_buffer_rsrc_t r, uint32_t v
     __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, (int)soff, 0);
 }
 
+__device__ inline uint2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    typedef int i32x2 __attribute__((ext_vector_type(2)));
+    const i32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, 0);
+    return make_uint2((uint32_t)v[0], (uint32_t)v[1]);
+}
+
+__device__ inline void buf_store8(uint2 x, __amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    typedef int i32x2 __attribute__((ext_vector_type(2)));
+    const i32x2 v = {(int)x.x, (int)x.y};
+    __builtin_amdgcn_raw_buffer_store_b64(v, r, (int)voff, (int)soff, 0);
+}
+
 __device__ inline float buf_load4f(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
 }
@@ -189,9 +201,13 @@ __host__ inline int64_t chunk_grid_blocks(int n_seqs, int n_heads, int64_t max_c
 //   G   : chunk-local cumulative gate                          [64], fp32
 //   SC  : state entering the chunk, B-operand order            [DV/16][DK/4] x 64 lanes, io type
 //   U   : U = U~ - W S, B-operand order                        [DV/16][16] x 64 lanes, io type
+//   P   : decayed causal Q K^T, per token tile the B operand of P^T (chunk
+//         rows permuted like KT)                              [4][16] x 64 lanes, io type
+//   QF  : queries, per token tile the B operand of Q^T (dk permuted like W)
+//                                                              [4][DK/4] x 64 lanes, io type
 // ---------------------------------------------------------------------------
 struct Workspace {
-    void *w, *kt, *sc, *u;
+    void *w, *kt, *sc, *u, *p, *qf;
     float *ut, *g;
 };
 
@@ -202,6 +218,8 @@ template <typename T, int DK, int DV> struct WsLayout {
     static constexpr size_t g_elems = kChunk;
     static constexpr size_t sc_elems = (size_t)DK * DV;
     static constexpr size_t u_elems = (size_t)kChunk * DV;
+    static constexpr size_t p_elems = (size_t)kChunk * kChunk;
+    static constexpr size_t qf_elems = (size_t)kChunk * DK;
 };
 
 }  // namespace la

@@ -60,6 +60,18 @@ int scan_variant(bool f32, int dk) {
 
 size_t io_size(int32_t dtype) { return dtype == LA_BF16 ? 2 : 4; }
 
+// Whether a call that runs the scan and output stages together uses the
+// single-wave scan's output wave (one kernel) instead of the split output
+// kernel; both give identical bits.  LA_SCAN_OUTPUT=0 selects the split
+// kernels (for measurement).
+bool scan_with_output() {
+    static const bool on = [] {
+        const char *e = getenv("LA_SCAN_OUTPUT");
+        return !(e && atoi(e) == 0);
+    }();
+    return on;
+}
+
 // Chunks per segment of the two-level scan (1 = single-level).  A segment
 // must divide a checkpoint interval's chunks, so every checkpoint position is
 // a segment boundary and a resume from a checkpoint sees the same segments
@@ -104,7 +116,7 @@ la_status check_shape(const la_shape *s) {
 }
 
 struct WsPlan {
-    size_t w, kt, ut, g, sc, u;              // byte offsets of each region
+    size_t w, kt, ut, g, sc, u, pm, qf;      // byte offsets of each region
     size_t phi, segr, segd, segst;           // two-level scan regions (seg_m >= 2)
     int seg_m;
     size_t total;
@@ -124,6 +136,8 @@ WsPlan plan_workspace(const la_shape *s, int64_t total_tokens) {
     p.g = take(sh * la::kChunk * sizeof(float));
     p.sc = take(sh * (size_t)s->dk * s->dv * io);
     p.u = take(sh * la::kChunk * s->dv * io);
+    p.pm = take(sh * la::kChunk * la::kChunk * io);
+    p.qf = take(sh * la::kChunk * s->dk * io);
     p.seg_m = seg_chunks(s);
     p.phi = p.segr = p.segd = p.segst = 0;
     if (p.seg_m > 1) {
@@ -160,10 +174,10 @@ la_status launch_out(const PrefillCall &c, const la::Workspace &ws, int64_t max_
     const int cps = la::chunks_per_interval(s->ckpt_interval);
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[2], c.stream);
     if (max_chunks > 0 && (c.stages & LA_STAGE_OUTPUT)) {
-        la::OutArgs oa{c.q, c.k, c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
+        la::OutArgs oa{c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
                        (int32_t)max_chunks, s->scale, ws};
         const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
-        hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(256), 0, c.stream, oa);
+        hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(4 * DV), 0, c.stream, oa);
         if (la_status e = hip_check("output launch")) return e;
     }
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[3], c.stream);
@@ -215,13 +229,15 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
     ws.g = (float *)(base + p.g);
     ws.sc = base + p.sc;
     ws.u = base + p.u;
+    ws.p = base + p.pm;
+    ws.qf = base + p.qf;
 
     const bool trace = g_trace_n >= 4;
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[0], c.stream);
     (void)hipGetLastError();
 
     if (max_chunks > 0 && (c.stages & LA_STAGE_PREPARE)) {
-        la::PrepArgs pa{c.k, c.v, c.g, c.beta, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
+        la::PrepArgs pa{c.q, c.k, c.v, c.g, c.beta, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
                         s->variant, (int32_t)max_chunks, ws};
         const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
         hipLaunchKernelGGL((la::gdr_prep_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(256), 0, c.stream, pa);
@@ -230,7 +246,8 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[1], c.stream);
     if (c.stages & LA_STAGE_SCAN) {
         la::ScanArgs sa{c.cu_dev, c.state_in, c.final_state, c.ckpt_out, c.ckpt_off_dev,
-                        s->n_seqs, s->n_heads, s->ckpt_interval, cps, ws, 1, 0, {}};
+                        s->n_seqs, s->n_heads, s->ckpt_interval, cps, ws, 1, 0, {},
+                        c.o, s->scale};
         constexpr int NT = DV / 16;
         const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
         const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
@@ -246,6 +263,13 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
                 if (la_status e = hip_check("inter-chunk scan launch")) return e;
                 return launch_out<T, DK, DV>(c, ws, max_chunks, trace);
             }
+        }
+        if (scan_variant(sizeof(T) == 4, DK) == 1 && (c.stages & LA_STAGE_OUTPUT) && scan_with_output()) {
+            // the scan's output wave produces the output: no output launch
+            hipLaunchKernelGGL((la::gdr_scan1o_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(128), 0,
+                               c.stream, sa);
+            if (la_status e = hip_check("inter-chunk scan launch")) return e;
+            return launch_out<T, DK, DV>(c, ws, 0, trace);
         }
         if (scan_variant(sizeof(T) == 4, DK) == 1)
             hipLaunchKernelGGL((la::gdr_scan1_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(64), 0,

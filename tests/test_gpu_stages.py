@@ -70,3 +70,24 @@ def test_resume_prepared_while_state_restores(C):
     torch.cuda.synchronize()
     assert torch.equal(r.o, ref.o) and torch.equal(r.final, ref.final_state) and torch.equal(r.ckpt, ref.ckpt)
     assert torch.equal(r.o, cold.o[B:]) and torch.equal(r.final, cold.final_state)
+
+
+@pytest.mark.parametrize("dk,dv,io", [(64, 64, wl.BF16), (64, 128, wl.BF16), (128, 64, wl.BF16), (128, 128, wl.BF16),
+                                      (64, 64, wl.F32), (64, 128, wl.F32)])
+def test_scan_output_wave_equals_split_output_kernel(dk, dv, io):
+    """One call with the scan and output stages together reads the output
+    out in the scan kernel's output wave; split calls run the output kernel
+    on the state and U the scan left in the workspace.  Same bits, on a
+    ragged varlen batch (partial last chunks, a 1-token and an empty
+    sequence)."""
+    lens = [1000, 0, 257, 64, 1]
+    C = 256 if io == wl.BF16 else 64
+    x = wl.random_inputs(90 + dk + dv, lens, 3, dk, dv, io_dtype=io, gate_scale=0.02)
+    xd = api.to_device(x)
+    ref = api.Prefill(xd, C).run()
+    p = api.Prefill(xd, C)
+    p.run(stages=P | S)
+    p.run(stages=O)
+    torch.cuda.synchronize()
+    res = api.PrefillResult(p.o, p.final, p.ckpt, p.ckpt_offsets, p.n_ckpt_rows)
+    assert _equal(ref, res)
