@@ -6,11 +6,13 @@ One step is one pass of the whole path over the one-TP-rank workload
 checkpoint interval C = 256):
 
   1. strict-prefix boundary on the host: B = 3,328 for N = 3,584;
-  2. cold prefill of all 3,584 tokens, emitting 14 fp32 checkpoints;
-  3. paged save of the 14 x 8 checkpoint pages into a pool through a
-     random-permutation page table;
-  4. paged restore of the 8 pages of the checkpoint at B;
-  5. resume over the 256-token suffix [B, N) from the restored state.
+  2. cold prefill of all 3,584 tokens, its 14 x 8 fp32 checkpoint pages
+     written straight into a pool through a random-permutation page table
+     (the paged save folded into the scan, la_prefill_paged);
+  3. resume over the 256-token suffix [B, N), its starting state read
+     straight from the 8 pages of the checkpoint at B (the paged restore
+     folded into the scan) and its checkpoint at N written to that
+     prefix's pages.
 
 Beside the step it reports, each on its own timer: paged save/restore
 bandwidth on the full 4,096-page pool, decode continuation (one token per
@@ -261,15 +263,17 @@ def main():
     B = la.strict_prefix_boundary(N, C, w.available[0])
     xd = api.to_device(x)
     xs = api.to_device(x.tokens(B, N))
-    cold = api.Prefill(xd, C)
-    resume = api.Prefill(xs, C, starts=[B])
+    cold = api.Prefill(xd, C, emit_ckpt=False)
+    resume = api.Prefill(xs, C, starts=[B], emit_ckpt=False)
     n_ck = cold.n_ckpt_rows
     rng = np.random.default_rng(11)
     pool = torch.empty((n_ck * H, dk * dv), dtype=torch.float32, device="cuda")
     save_ids = torch.from_numpy(rng.permutation(n_ck * H).astype(np.int32)).cuda()
     j = B // C - 1
+    # the resume starts from the page of prefix B and writes the checkpoint
+    # pages of its own prefixes (B + C, ...): the cold run's pages for those
     restore_ids = save_ids[j * H:(j + 1) * H].contiguous()
-    restored = torch.empty((1, H, dk, dv), dtype=torch.float32, device="cuda")
+    resume_ck_ids = save_ids[(j + 1) * H:(j + 1 + resume.n_ckpt_rows) * H].contiguous()
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     ev = HipEvents(10)
@@ -280,12 +284,12 @@ def main():
         assert b == B
         if trace:
             la.la_trace_set_events(stage_ev)
-        cold.run()
+        # cold prefill: checkpoints straight into the pool's pages (the save)
+        cold.run_paged(pool, ckpt_page_ids=save_ids)
         if trace:
             la.la_trace_set_events([])
-        la.la_state_save_paged(cold.ckpt, pool, save_ids)
-        la.la_state_restore_paged(pool, restore_ids, restored)
-        resume.run(restored)
+        # reload: the resume reads its starting state straight from the page (the restore)
+        resume.run_paged(pool, ckpt_page_ids=resume_ck_ids, state_page_ids=restore_ids)
 
     for _ in range(args.warmup):
         step(False)

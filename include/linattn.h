@@ -164,11 +164,13 @@ la_status la_prefill_resume(const la_shape *shape,
  * restored (section 3.1), and one call's output can run beside the next
  * call's scan.  `stages` is a mask of
  *   LA_STAGE_PREPARE (1): chunk-local gate sums and the intra-chunk operands
- *                         (from k, v, g, beta) into the workspace;
+ *                         (from q, k, v, g, beta) into the workspace;
  *   LA_STAGE_SCAN    (2): the inter-chunk recurrence from state_in (or zero):
  *                         checkpoints and the final state, plus the per-chunk
  *                         states the output needs, into the workspace;
- *   LA_STAGE_OUTPUT  (4): o from q, k and the workspace.
+ *   LA_STAGE_OUTPUT  (4): o from the workspace.
+ * A call that runs SCAN and OUTPUT together computes o inside the scan
+ * kernel; split calls compute the same o bit for bit.
  * Arguments as la_prefill_resume; start_pos_dev/host NULL make it a cold
  * call, and then state_in must be NULL.  Every call validates all arguments.
  * The stages of one call must run in that order on one workspace with the
@@ -189,6 +191,50 @@ la_status la_prefill_stages(const la_shape *shape, uint32_t stages,
                             float *ckpt_out, const int32_t *ckpt_offsets_dev,
                             const int32_t *ckpt_offsets_host,
                             void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * la_prefill_paged - a prefill (cold or resumed) whose checkpoints go
+ * straight into pool pages and whose starting states come straight from pool
+ * pages: the save of section 3.1 and the restore of a reload (sections 3.2
+ * and 5.5, Table 5) folded into the prefill, with the pool and page layout
+ * of la_state_save_paged / la_state_restore_paged (one page = one head's
+ * [dk, dv] fp32 state).
+ *
+ *   pages->pool            device fp32 [n_pages, dk*dv], 16-byte aligned.
+ *   pages->ckpt_page_ids   device int32 [rows * H] or NULL (no checkpoints):
+ *                          checkpoint row r, head h (rows numbered by
+ *                          ckpt_offsets exactly as ckpt_out's in
+ *                          la_prefill_resume) is written to page
+ *                          ckpt_page_ids[r * H + h]; -1 writes nothing.
+ *   pages->state_page_ids  device int32 [n_seqs * H], required with
+ *                          start_pos (a resume), NULL for a cold call:
+ *                          (sequence i, head h) starts from page
+ *                          state_page_ids[i * H + h], the state for prefix
+ *                          [0, B_i); -1 starts from the zero state (B_i = 0).
+ *   pages->err_count       device int32 or NULL: incremented once per page
+ *                          id outside [-1, n_pages).  Such a checkpoint is
+ *                          not written; such a start uses the zero state.
+ * start_pos_dev/host NULL make a cold call.  ckpt_offsets are required with
+ * ckpt_page_ids.  The pool must not alias the other buffers; a page read as
+ * a starting state must not also be written as a checkpoint in the same
+ * call.  Other arguments, results and errors as la_prefill_resume.
+ */
+typedef struct {
+    float *pool;
+    int64_t n_pages;
+    const int32_t *ckpt_page_ids;
+    const int32_t *state_page_ids;
+    int32_t *err_count;
+} la_pages;
+
+la_status la_prefill_paged(const la_shape *shape, const la_pages *pages,
+                           const void *q, const void *k, const void *v,
+                           const float *g, const float *beta,
+                           const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                           const int64_t *start_pos_dev, const int64_t *start_pos_host,
+                           void *o, float *final_state,
+                           const int32_t *ckpt_offsets_dev, const int32_t *ckpt_offsets_host,
+                           void *workspace, size_t ws_bytes, void *stream);
 
 /*
  * la_decode_step - decode continuation: advance every (sequence, head) by one

@@ -136,6 +136,21 @@ class Prefill:
         return PrefillResult(self.o, self.final, ck, self.ckpt_offsets, self.n_ckpt_rows)
 
 
+    def run_paged(self, pool: torch.Tensor, ckpt_page_ids: Optional[torch.Tensor] = None,
+                  state_page_ids: Optional[torch.Tensor] = None, err_count: Optional[torch.Tensor] = None,
+                  stream=None) -> PrefillResult:
+        """la_prefill_paged: checkpoints to pool pages (rows numbered as
+        ckpt_offsets), starting states from pool pages (a resume).  The
+        result's ckpt is None: the checkpoints live in the pool."""
+        x = self.x
+        pages = la.make_pages(pool, ckpt_page_ids, state_page_ids, err_count)
+        with_ck = ckpt_page_ids is not None
+        la.la_prefill_paged(self.shape, pages, x.q, x.k, x.v, x.g, x.beta, x.cu_dev, x.cu_host, self.start_dev,
+                            self.starts, self.o, self.final, self.ckpt_off_dev if with_ck else None,
+                            self.ckpt_offsets if with_ck else None, self.workspace, stream)
+        return PrefillResult(self.o, self.final, None, self.ckpt_offsets, self.n_ckpt_rows)
+
+
 def prefill(x: DeviceInputs, interval: int, variant: int = la.LA_GDR_LITERAL, scale: float = 1.0,
             emit_ckpt: bool = True) -> PrefillResult:
     return Prefill(x, interval, variant, scale, None, emit_ckpt).run()

@@ -1,11 +1,9 @@
-// Workgroup forms of the chunk scan, for throughput: the chunk operands
-// (-W and K~^T, 32 KB per chunk at dk = 128) are read from HBM/L2 once per
-// workgroup and shared through LDS, instead of once per 16-column wave.
+// Workgroup forms of the chunk scan for the two-level scan's parallel
+// levels, for throughput: the chunk operands (-W and K~^T, 32 KB per chunk
+// at dk = 128) are read from HBM/L2 once per workgroup and shared through
+// LDS, instead of once per 16-column wave.
 //
 // A workgroup owns one unit of state columns:
-//   kGroupFull    (sequence, head), DV columns, the whole sequence: the state
-//                 entering each chunk and U for the output kernel,
-//                 checkpoints and the final state;
 //   kGroupTrans   (sequence, head, segment), DK + DV columns of [Phi | R]
 //                 started from [I | 0]: the segment's state map;
 //   kGroupReplay  (sequence, head, segment), DV columns from the segment's
@@ -24,7 +22,7 @@
 
 namespace la {
 
-enum : int { kGroupFull = 0, kGroupTrans = 1, kGroupReplay = 2 };
+enum : int { kGroupTrans = 1, kGroupReplay = 2 };
 constexpr int kGroupWaves = 4;
 
 template <typename T, int DK> struct GroupOps {
@@ -53,7 +51,6 @@ __global__ __launch_bounds__(64 * kGroupWaves) void gdr_group_kernel(ScanArgs a)
     constexpr int kLoads = PW + 1 + 4 * (TPW - NPHI);                  // global loads per chunk
 
     __shared__ uint4 ops_lds[2][NV][64];
-    __shared__ float tr_lds[kGroupWaves][MODE == kGroupFull ? DK * kTrLd : 1];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -65,33 +62,21 @@ __global__ __launch_bounds__(64 * kGroupWaves) void gdr_group_kernel(ScanArgs a)
     int64_t base, seg_slot = 0;
     {
         const int unit = blockIdx.x;
-        if (MODE == kGroupFull) {
-            if (unit >= a.n_seqs * H) return;
-            seq = unit / H;
-            h = unit % H;
-        } else {
-            const int pair = unit / a.max_seg;
-            seg = unit % a.max_seg;
-            if (pair >= a.n_seqs * H) return;
-            seq = pair / H;
-            h = pair % H;
-        }
+        const int pair = unit / a.max_seg;
+        seg = unit % a.max_seg;
+        if (pair >= a.n_seqs * H) return;
+        seq = pair / H;
+        h = pair % H;
         const int cu0 = a.cu[seq];
         len = a.cu[seq + 1] - cu0;
         nch = n_chunks32(len, a.C, a.cps);
         base = slot_base(cu0, seq, a.C, a.cps);
-        if (MODE == kGroupFull) {
-            c0 = 0;
-            c1 = nch;
-        } else {
-            c0 = seg * a.seg_m;
-            if (c0 >= nch) return;
-            c1 = min(c0 + a.seg_m, nch);
-            seg_slot = slot_base(cu0, seq, (int64_t)a.C * a.seg_m, a.cps) + seg;
-        }
+        c0 = seg * a.seg_m;
+        if (c0 >= nch) return;
+        c1 = min(c0 + a.seg_m, nch);
+        seg_slot = slot_base(cu0, seq, (int64_t)a.C * a.seg_m, a.cps) + seg;
     }
     const int n = c1 - c0;
-    const size_t pair_off = ((size_t)seq * H + h) * DK * DV;
 
     // ---- initial state of every tile
     f32x4 S[TPW][RT];
@@ -108,14 +93,12 @@ __global__ __launch_bounds__(64 * kGroupWaves) void gdr_group_kernel(ScanArgs a)
 #pragma unroll
             for (int t = 0; t < RT; ++t) S[i][t] = zero4();
         } else {
-            if (MODE == kGroupFull || seg == 0)
-                load_state_tile<DK, DV>(a.state_in ? a.state_in + pair_off : nullptr, tile, S[i]);
+            if (seg == 0)   // (bad page ids are counted by the combine kernel)
+                load_state_tile<DK, DV>(start_state(a, seq, h, (size_t)DK * DV, false), tile, S[i]);
             else
                 load_state_c<RT>(a.seg.state + (seg_slot * H + h) * DK * DV, tile, S[i]);
         }
     }
-    ChunkCursor cur{0, a.C, len, a.C};
-    int ckpt_row = (MODE == kGroupFull && a.ckpt) ? a.ckpt_off[seq] : 0;
     float dprod = 1.f;
     const uint32_t lane16 = 16u * (uint32_t)lane;
     __builtin_amdgcn_s_waitcnt(0);
@@ -239,17 +222,6 @@ __global__ __launch_bounds__(64 * kGroupWaves) void gdr_group_kernel(ScanArgs a)
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                   // MFMA
             if (q < kLoads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
         }
-        if constexpr (MODE == kGroupFull) {
-            if (cur.advance()) {
-                const int row = ckpt_row++;
-                if (a.ckpt) {
-#pragma unroll
-                    for (int i = 0; i < TPW; ++i)
-                        store_state_tiles_t<RT, DV>(a.ckpt + ((size_t)row * H + h) * DK * DV + 16 * (i * kGroupWaves + w),
-                                                    S[i], tr_lds[w]);
-                }
-            }
-        }
     };
 
     // ---- pipeline: operands of chunk j in LDS buffer j & 1
@@ -281,13 +253,7 @@ __global__ __launch_bounds__(64 * kGroupWaves) void gdr_group_kernel(ScanArgs a)
     if (j < n) step(oA, 0, j);
 
     // ---- epilogue
-    if constexpr (MODE == kGroupFull) {
-        if (a.final_state) {
-#pragma unroll
-            for (int i = 0; i < TPW; ++i)
-                store_state_tiles_t<RT, DV>(a.final_state + pair_off + 16 * (i * kGroupWaves + w), S[i], tr_lds[w]);
-        }
-    } else if constexpr (MODE == kGroupTrans) {
+    if constexpr (MODE == kGroupTrans) {
         const int64_t ssh = seg_slot * H + h;
 #pragma unroll
         for (int i = 0; i < TPW; ++i) {

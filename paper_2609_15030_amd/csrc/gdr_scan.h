@@ -39,6 +39,18 @@ struct SegWorkspace {
     float *state;     // state entering the segment, fp32 C-layout tiles (segments >= 1)
 };
 
+// Paged state I/O: checkpoints written straight into pool pages and the
+// starting state read straight from one (the page save and restore of a
+// reload folded into the scan).
+struct PageIO {
+    float *pool;                  // [n_pages][DK * DV] fp32, or null
+    const int32_t *ckpt_ids;      // page of checkpoint row r, head h at [r * H + h] (-1: not written), or null
+    const int32_t *state_ids;     // page of the state (sequence i, head h) starts from at [i * H + h]
+                                  // (-1: zero state), or null
+    int32_t *err;                 // optional: +1 per id outside [-1, n_pages)
+    int32_t n_pages;
+};
+
 struct ScanArgs {
     const int32_t *cu;
     const float *state_in;        // [n_seqs, H, DK, DV] or null (zero state)
@@ -51,6 +63,79 @@ struct ScanArgs {
     SegWorkspace seg;
     void *o;                      // scan with output wave only: output [T, H, dv] (io type)
     float scale;
+    PageIO pg;
+};
+
+// Counts an id outside [-1, n_pages) once: count is set in one wave per
+// (sequence, head), and one lane adds.
+__device__ inline void count_bad_id(const PageIO &pg, int id, bool count) {
+    if (count && pg.err && (id < -1 || id >= pg.n_pages) && (threadIdx.x & 63) == 0) atomicAdd(pg.err, 1);
+}
+
+// The state (sequence seq, head h) starts from: its rows of state_in, the
+// pool page the state page table names, or null for the zero state (no
+// state_in; page id -1; a page id out of range, which is counted).
+__device__ inline const float *start_state(const ScanArgs &a, int seq, int h, size_t elems, bool count) {
+    const size_t item = (size_t)seq * a.n_heads + h;
+    if (a.pg.state_ids) {
+        const int id = a.pg.state_ids[item];
+        count_bad_id(a.pg, id, count);
+        return (id >= 0 && id < a.pg.n_pages) ? a.pg.pool + (size_t)id * elems : nullptr;
+    }
+    return a.state_in ? a.state_in + item * elems : nullptr;
+}
+
+// Destinations of the checkpoints of one (sequence, head), in order: rows
+// row0, row0 + 1, ... of the dense array, or the pool pages the checkpoint
+// page table names for those rows (null: not written).  A page id is read
+// with the operands of the chunk (or segment) that ends on its checkpoint,
+// load_id(row) in the operand prefetch, so no checkpoint waits on a read.
+struct CkptDst {
+    float *dense, *pool;
+    int32_t *err;
+    __amdgpu_buffer_rsrc_t ids;   // this (sequence, head)'s page ids, stride H (no records when dense)
+    size_t elems;
+    int H, n_pages, n_rows, k;
+    bool paged, count;
+
+    __device__ void init(const ScanArgs &a, int seq, int h, int len, size_t E, bool cnt) {
+        H = a.n_heads;
+        elems = E;
+        count = cnt;
+        pool = a.pg.pool;
+        err = a.pg.err;
+        n_pages = a.pg.n_pages;
+        n_rows = len / a.C;               // positions are local and start on a multiple of C
+        k = 0;
+        paged = a.pg.ckpt_ids != nullptr;
+        dense = (!paged && a.ckpt) ? a.ckpt + ((size_t)a.ckpt_off[seq] * H + h) * E : nullptr;
+        const int32_t *base = paged ? a.pg.ckpt_ids + (size_t)a.ckpt_off[seq] * H + h : a.pg.ckpt_ids;
+        // the values are wave-uniform; readfirstlane keeps the resource in
+        // scalar registers (a vector-register resource costs a loop per read)
+        const uint64_t bp = (uint64_t)base;
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)bp);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(bp >> 32));
+        const uint32_t bytes = (uint32_t)__builtin_amdgcn_readfirstlane(paged ? n_rows * H * 4 : 0);
+        ids = make_rsrc((const void *)(((uint64_t)hi << 32) | lo), bytes);
+    }
+    // Issues the read of the page id of local checkpoint row r (uniform; rows
+    // past the last read as 0 and are never used).
+    __device__ int load_id(int r) const {
+        return __builtin_amdgcn_raw_buffer_load_b32(ids, (int)((uint32_t)r * (uint32_t)H * 4u), 0, 0);
+    }
+    // Destination of the next checkpoint; id is load_id() of its row.
+    __device__ float *next(int id) {
+        float *d = nullptr;
+        if (paged) {
+            id = __builtin_amdgcn_readfirstlane(id);
+            if (count && err && (id < -1 || id >= n_pages) && (threadIdx.x & 63) == 0) atomicAdd(err, 1);
+            if (id >= 0 && id < n_pages) d = pool + (size_t)id * elems;
+        } else if (dense) {
+            d = dense + (size_t)k * H * elems;
+        }
+        ++k;
+        return d;
+    }
 };
 
 // Chunk bounds of one sequence, advanced by additions only (the plan of
@@ -202,18 +287,20 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
 
     // this wave's state rows: tiles 2w and 2w + 1
     f32x4 S[2];
-    if (a.state_in) {
+    const float *src = start_state(a, seq, h, (size_t)DK * DV, tile == 0 && w == 0);
+    if (src) {
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                S[t][i] = a.state_in[state_off + (size_t)(32 * w + 16 * t + 4 * g16 + i) * DV + col];
+                S[t][i] = src[(size_t)(32 * w + 16 * t + 4 * g16 + i) * DV + col];
     } else {
         S[0] = zero4();
         S[1] = zero4();
     }
     ChunkCursor cur{0, a.C, len, a.C};
-    int ckpt_row = a.ckpt ? a.ckpt_off[seq] : 0;
+    CkptDst ck;
+    ck.init(a, seq, h, len, (size_t)DK * DV, tile == 0 && w == 0);
     const uint32_t lane_off = 4u * (uint32_t)(4 * g16 * DV + col);   // C-layout store offset
     // Drain the counters once here: without it the waitcnt pass sees the
     // state loads as possibly pending at the loop header and waits on the
@@ -225,6 +312,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
         uint4 kt[2][VU];      // K~^T rows of this wave's 2 dk tiles, all chunk rows
         f32x4 ut[MTW];        // U~ row tiles this wave reduces
         float gl;             // G_63
+        int ckid;             // page id of the checkpoint this chunk would end (paged)
     };
     const uint32_t lane16 = 16u * (uint32_t)lane;
     auto load = [&](Ops &o, int jj) {
@@ -232,6 +320,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
         // issue order: gate, U~, -W, K~^T (earliest-needed last is fine: each
         // use waits only for the loads issued before it)
         o.gl = buf_load4f(make_rsrc(a.ws.g + sh * kChunk, kChunk * sizeof(float)), 0u, 4u * (kChunk - 1));
+        o.ckid = ck.load_id(jj / a.cps);
         const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
 #pragma unroll
         for (int m = 0; m < MTW; ++m) {
@@ -316,10 +405,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
         }
         // checkpoint when the chunk ends on a multiple of C
         if (cur.advance()) {
-            const int row = ckpt_row++;
-            if (a.ckpt)
-                store_state_tiles<2, DV>(a.ckpt + ((size_t)row * H + h) * DK * DV + (size_t)32 * w * DV, S,
-                                         lane_off);
+            if (float *d = ck.next(o.ckid)) store_state_tiles<2, DV>(d + (size_t)32 * w * DV, S, lane_off);
         }
     };
 
@@ -355,11 +441,14 @@ __device__ inline void lds_barrier() {
 // state update, with the next chunk's operands in flight while one is
 // computed.  scan1_chunks runs the whole sequence of one (sequence, head) on
 // one tile and writes the checkpoints.  It hands the state entering each
-// chunk and U to the split output kernel through the workspace or, with hs
-// set, to the workgroup's output wave through LDS (one barrier per chunk).
-template <typename T, int DK, int DV>
+// chunk and U to the split output kernel through the workspace or, with
+// HANDOFF, to the workgroup's output wave through the LDS slots hs (one
+// barrier per chunk).  HANDOFF is a compile-time choice: a run-time test
+// would split a chunk's step into several basic blocks, and the load/MFMA
+// interleave below is scheduled within one block.
+template <typename T, int DK, int DV, bool HANDOFF>
 __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile, int len, int64_t base,
-                                    int nch, f32x4 (&S)[DK / 16], Handoff<T, DK> *hs = nullptr) {
+                                    int nch, f32x4 (&S)[DK / 16], Handoff<T, DK> *hs) {
     using M = MT<T>;
     using L = WsLayout<T, DK, DV>;
     constexpr int KW = M::KW, VEC = Vec<T>::N;
@@ -373,7 +462,8 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
     const int lane = threadIdx.x & 63, g16 = lane >> 4, c16 = lane & 15;
     const int H = a.n_heads;
     ChunkCursor cur{0, a.C, len, a.C};
-    int ckpt_row = a.ckpt ? a.ckpt_off[seq] : 0;
+    CkptDst ck;
+    ck.init(a, seq, h, len, (size_t)DK * DV, tile == 0);
     const uint32_t lane_off = 4u * (uint32_t)(4 * g16 * DV + 16 * tile + c16);
     // Drain the counters once here: without it the waitcnt pass sees the
     // state loads as possibly pending at the loop header and waits on the
@@ -382,6 +472,7 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
 
     struct Ops {
         float gl;
+        int ckid;             // page id of the checkpoint this chunk would end (paged)
         f32x4 ut[4];
         uint4 wn[4][VS];
         uint4 kt[RT][VU];
@@ -390,6 +481,7 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
     auto load = [&](Ops &o, int jj) {
         const int64_t sh = (base + jj) * H + h;
         o.gl = buf_load4f(make_rsrc(a.ws.g + sh * kChunk, kChunk * sizeof(float)), 0u, 4u * (kChunk - 1));
+        o.ckid = ck.load_id(jj / a.cps);
         const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
@@ -412,7 +504,7 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
         T sb[FS];
 #pragma unroll
         for (int f = 0; f < FS; ++f) sb[f] = from_f32<T>(S[f >> 2][f & 3]);
-        if (hs) {
+        if constexpr (HANDOFF) {
 #pragma unroll
             for (int v = 0; v < VS; ++v) hs->sb[jj & 1][v][lane] = *(const uint4 *)&sb[v * VEC];
         } else {
@@ -434,7 +526,7 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
         T ub[FU];
 #pragma unroll
         for (int f = 0; f < FU; ++f) ub[f] = from_f32<T>(U[f >> 2][f & 3]);
-        if (hs) {
+        if constexpr (HANDOFF) {
 #pragma unroll
             for (int v = 0; v < VU; ++v) hs->ub[jj & 1][v][lane] = *(const uint4 *)&ub[v * VEC];
         } else {
@@ -465,10 +557,9 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
         }
         if (kLoads > kMfmas) __builtin_amdgcn_sched_group_barrier(0x020, kLoads - kMfmas, 0);
         if (cur.advance()) {
-            const int row = ckpt_row++;
-            if (a.ckpt) store_state_tiles<RT, DV>(a.ckpt + ((size_t)row * H + h) * DK * DV, S, lane_off);
+            if (float *d = ck.next(o.ckid)) store_state_tiles<RT, DV>(d, S, lane_off);
         }
-        if (hs) lds_barrier();   // this chunk's slot is written; the output wave may read it
+        if constexpr (HANDOFF) lds_barrier();   // this chunk's slot is written; the output wave may read it
     };
     scan_ring<1>(nch, load, step, (Ops *)nullptr);
 }
@@ -533,8 +624,8 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
     const int64_t base = slot_base(cu0, seq, a.C, a.cps);
     const size_t state_off = (size_t)pair * DK * DV;
     f32x4 S[DK / 16];
-    load_state_tile<DK, DV>(a.state_in ? a.state_in + state_off : nullptr, tile, S);
-    scan1_chunks<T, DK, DV>(a, seq, h, tile, len, base, nch, S);
+    load_state_tile<DK, DV>(start_state(a, seq, h, (size_t)DK * DV, tile == 0), tile, S);
+    scan1_chunks<T, DK, DV, false>(a, seq, h, tile, len, base, nch, S, nullptr);
     if (a.final_state) {
         const int lane = threadIdx.x;
         store_state_tiles<DK / 16, DV>(a.final_state + state_off, S,
@@ -563,8 +654,8 @@ __global__ __launch_bounds__(128) void gdr_scan1o_kernel(ScanArgs a) {
     if (wave == 0) {
         const size_t state_off = (size_t)pair * DK * DV;
         f32x4 S[DK / 16];
-        load_state_tile<DK, DV>(a.state_in ? a.state_in + state_off : nullptr, tile, S);
-        scan1_chunks<T, DK, DV>(a, seq, h, tile, len, base, nch, S, &hs);
+        load_state_tile<DK, DV>(start_state(a, seq, h, (size_t)DK * DV, tile == 0), tile, S);
+        scan1_chunks<T, DK, DV, true>(a, seq, h, tile, len, base, nch, S, &hs);
         if (a.final_state) {
             const int lane = threadIdx.x & 63;
             store_state_tiles<DK / 16, DV>(a.final_state + state_off, S,
@@ -608,19 +699,22 @@ __global__ __launch_bounds__(64) void gdr_seg_combine_kernel(ScanArgs a) {
     const size_t state_off = (size_t)pair * DK * DV;
     __shared__ float tr_lds[DK * kTrLd];
     f32x4 S[RT];
-    load_state_tile<DK, DV>(a.state_in ? a.state_in + state_off : nullptr, tile, S);
-    const int ckpt0 = a.ckpt ? a.ckpt_off[seq] : 0;
+    load_state_tile<DK, DV>(start_state(a, seq, h, (size_t)DK * DV, tile == 0), tile, S);
+    CkptDst ck;
+    ck.init(a, seq, h, len, (size_t)DK * DV, tile == 0);
     const uint32_t lane16 = 16u * (uint32_t)lane;
     const uint32_t phi_lane = (uint32_t)((c16 * DK + 8 * g16) * sizeof(T));
     __builtin_amdgcn_s_waitcnt(0);
 
     struct Ops {
         float d;
+        int ckid;             // page id of the checkpoint this segment would end (paged)
         f32x4 r[RT];
         uint4 ph[RT][VS];
     };
     auto load = [&](Ops &o, int sg) {
         const int64_t ssh = (sbase + sg) * H + h;
+        o.ckid = ck.load_id(max((sg + 1) * a.seg_m / a.cps - 1, 0));
         o.d = buf_load4f(make_rsrc(a.seg.d + ssh, sizeof(float)), 0u, 0u);
         const auto rr = make_rsrc(a.seg.r + ssh * DK * DV, DK * DV * sizeof(float));
 #pragma unroll
@@ -657,9 +751,9 @@ __global__ __launch_bounds__(64) void gdr_seg_combine_kernel(ScanArgs a) {
         int lo, hi;
         chunk_range32(min((sg + 1) * a.seg_m, nch) - 1, len, a.C, a.cps, &lo, &hi);
         if (sg + 1 < nseg) store_state_c<RT>(a.seg.state + ((sbase + sg + 1) * H + h) * DK * DV, tile, S);
-        if (hi % a.C == 0 && a.ckpt)
-            store_state_tiles_t<RT, DV>(a.ckpt + ((size_t)(ckpt0 + hi / a.C - 1) * H + h) * DK * DV + 16 * tile, S,
-                                        tr_lds);
+        if (hi % a.C == 0) {   // checkpoints come in order, one per C-aligned segment end
+            if (float *d = ck.next(o.ckid)) store_state_tiles_t<RT, DV>(d + 16 * tile, S, tr_lds);
+        }
     };
     scan_ring<1>(nseg, load, step, (Ops *)nullptr);
     if (a.final_state) store_state_tiles_t<RT, DV>(a.final_state + state_off + 16 * tile, S, tr_lds);

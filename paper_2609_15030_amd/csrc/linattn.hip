@@ -166,6 +166,7 @@ struct PrefillCall {
     size_t ws_bytes;
     hipStream_t stream;
     uint32_t stages = LA_STAGE_ALL;
+    const la_pages *pages = nullptr;         // paged checkpoints / starting states
 };
 
 template <typename T, int DK, int DV>
@@ -247,22 +248,19 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
     if (c.stages & LA_STAGE_SCAN) {
         la::ScanArgs sa{c.cu_dev, c.state_in, c.final_state, c.ckpt_out, c.ckpt_off_dev,
                         s->n_seqs, s->n_heads, s->ckpt_interval, cps, ws, 1, 0, {},
-                        c.o, s->scale};
+                        c.o, s->scale, {}};
+        if (c.pages) {
+            sa.pg.pool = c.pages->pool;
+            sa.pg.ckpt_ids = c.pages->ckpt_page_ids;
+            sa.pg.state_ids = c.pages->state_page_ids;
+            sa.pg.err = c.pages->err_count;
+            sa.pg.n_pages = (int32_t)c.pages->n_pages;
+        }
         constexpr int NT = DV / 16;
         const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
         const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
         if constexpr (sizeof(T) == 2) {
             if (p.seg_m > 1) return launch_two_level<T, DK, DV>(c, p, sa, max_chunks, trace);
-            static const bool group = [] {
-                const char *e = getenv("LA_SCAN_GROUP");
-                return e && atoi(e) == 1;
-            }();
-            if (group) {
-                hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupFull>), dim3((unsigned)pairs),
-                                   dim3(64 * la::kGroupWaves), 0, c.stream, sa);
-                if (la_status e = hip_check("inter-chunk scan launch")) return e;
-                return launch_out<T, DK, DV>(c, ws, max_chunks, trace);
-            }
         }
         if (scan_variant(sizeof(T) == 4, DK) == 1 && (c.stages & LA_STAGE_OUTPUT) && scan_with_output()) {
             // the scan's output wave produces the output: no output launch
@@ -311,9 +309,23 @@ la_status run_prefill(const PrefillCall &c) {
         max_chunks = std::max(max_chunks, la::n_chunks(len, C, cps));
     }
     const int64_t total = c.cu_host[s->n_seqs];
+    if (c.pages) {
+        const la_pages *pg = c.pages;
+        if (c.state_in || c.ckpt_out) return fail(LA_ERR_INVALID_ARG, "internal: paged call with dense state I/O");
+        if (pg->n_pages < 0 || pg->n_pages > 0x7fffffff)
+            return fail(LA_ERR_INVALID_ARG, "n_pages=%lld", (long long)pg->n_pages);
+        if ((pg->ckpt_page_ids || pg->state_page_ids) && (!pg->pool || !aligned16(pg->pool)))
+            return fail(LA_ERR_INVALID_ARG, "pages->pool is required (16-byte aligned) with page ids");
+        if (pg->state_page_ids && !resume)
+            return fail(LA_ERR_INVALID_ARG, "state_page_ids given without start positions");
+        if (resume && !pg->state_page_ids)
+            return fail(LA_ERR_INVALID_ARG, "state_page_ids are required for a resume");
+        if (pg->ckpt_page_ids && (!c.ckpt_off_dev || !c.ckpt_off_host))
+            return fail(LA_ERR_INVALID_ARG, "ckpt_offsets_dev and ckpt_offsets_host are required with ckpt_page_ids");
+    }
     if (resume) {
         if (!c.start_host || !c.start_dev) return fail(LA_ERR_INVALID_ARG, "start_pos_dev and start_pos_host are required");
-        if (!c.state_in) return fail(LA_ERR_INVALID_ARG, "state_in is required for a resume");
+        if (!c.state_in && !c.pages) return fail(LA_ERR_INVALID_ARG, "state_in is required for a resume");
         for (int i = 0; i < s->n_seqs; ++i) {
             const int64_t B = c.start_host[i];
             const int64_t len = (int64_t)c.cu_host[i + 1] - c.cu_host[i];
@@ -348,6 +360,8 @@ la_status run_prefill(const PrefillCall &c) {
         if (!aligned16(c.ckpt_out)) return fail(LA_ERR_INVALID_ARG, "ckpt_out must be 16-byte aligned");
         if (!c.ckpt_off_dev || !c.ckpt_off_host)
             return fail(LA_ERR_INVALID_ARG, "ckpt_offsets_dev and ckpt_offsets_host are required with ckpt_out");
+    }
+    if (c.ckpt_out || (c.pages && c.pages->ckpt_page_ids)) {
         for (int i = 0; i < s->n_seqs; ++i)
             if (c.ckpt_off_host[i] < 0) return fail(LA_ERR_INVALID_ARG, "ckpt_offsets[%d] < 0", i);
     }
@@ -488,6 +502,21 @@ la_status la_prefill_stages(const la_shape *shape, uint32_t stages, const void *
     PrefillCall c{shape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host, start_pos_dev, start_pos_host,
                   state_in, o, final_state, ckpt_out, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
                   (hipStream_t)stream, stages};
+    return run_prefill(c);
+}
+
+la_status la_prefill_paged(const la_shape *shape, const la_pages *pages, const void *q, const void *k, const void *v,
+                           const float *g, const float *beta, const int32_t *cu_seqlens_dev,
+                           const int32_t *cu_seqlens_host, const int64_t *start_pos_dev,
+                           const int64_t *start_pos_host, void *o, float *final_state,
+                           const int32_t *ckpt_offsets_dev, const int32_t *ckpt_offsets_host, void *workspace,
+                           size_t ws_bytes, void *stream) {
+    if (!pages) return fail(LA_ERR_INVALID_ARG, "pages is NULL");
+    if ((start_pos_dev == nullptr) != (start_pos_host == nullptr))
+        return fail(LA_ERR_INVALID_ARG, "start_pos_dev and start_pos_host go together");
+    PrefillCall c{shape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host, start_pos_dev, start_pos_host,
+                  nullptr, o, final_state, nullptr, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
+                  (hipStream_t)stream, LA_STAGE_ALL, pages};
     return run_prefill(c);
 }
 

@@ -32,7 +32,8 @@ LA_GDR_LITERAL = 0
 LA_GDR_DECAYED_DELTA = 1
 
 EXPORTED = ("strict_prefix_boundary", "la_prefill_workspace_bytes", "la_prefill",
-            "la_prefill_resume", "la_prefill_stages", "la_decode_step", "la_state_save_paged", "la_state_restore_paged",
+            "la_prefill_resume", "la_prefill_stages", "la_prefill_paged", "la_decode_step", "la_state_save_paged",
+            "la_state_restore_paged",
             "la_state_save_host", "la_state_restore_host",
             "la_status_string", "la_last_error_message", "la_trace_set_events")
 
@@ -43,6 +44,12 @@ class LaShape(ctypes.Structure):
                 ("chunk", ctypes.c_int32), ("ckpt_interval", ctypes.c_int32),
                 ("io_dtype", ctypes.c_int32), ("variant", ctypes.c_int32),
                 ("scale", ctypes.c_float)]
+
+
+class LaPages(ctypes.Structure):
+    _fields_ = [("pool", ctypes.c_void_p), ("n_pages", ctypes.c_int64),
+                ("ckpt_page_ids", ctypes.c_void_p), ("state_page_ids", ctypes.c_void_p),
+                ("err_count", ctypes.c_void_p)]
 
 
 def make_shape(n_seqs, n_heads, dk, dv, ckpt_interval, io_dtype=LA_BF16,
@@ -74,6 +81,7 @@ def _load() -> ctypes.CDLL:
         "la_prefill": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_prefill_resume": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_prefill_stages": ([SH, ctypes.c_uint32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "la_prefill_paged": ([SH, ctypes.POINTER(LaPages), P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_decode_step": ([SH, P, P, P, P, P, P, P, P], I32),
         "la_state_save_paged": ([P, I64, I64, P, I64, P, P, P], I32),
         "la_state_restore_paged": ([P, I64, P, P, I64, I64, P, P], I32),
@@ -233,6 +241,30 @@ def la_prefill_stages(shape: LaShape, stages: int, q, k, v, g, beta, cu_dev, cu_
                                 _hptr(sh, np.int64), _dptr(state_in), _dptr(o), _dptr(final_state),
                                 _dptr(ckpt_out), _dptr(ckpt_off_dev), _hptr(oh, np.int32), _dptr(workspace),
                                 workspace.numel() * workspace.element_size(), _stream(stream))
+    if check:
+        _check(st)
+    return st
+
+
+def make_pages(pool, ckpt_page_ids=None, state_page_ids=None, err_count=None, n_pages=None) -> LaPages:
+    """la_pages for a device pool ([n_pages, dk * dv] fp32) and device int32 page tables."""
+    n = pool.shape[0] if n_pages is None else n_pages
+    return LaPages(_dptr(pool), int(n), _dptr(ckpt_page_ids), _dptr(state_page_ids), _dptr(err_count))
+
+
+def la_prefill_paged(shape: LaShape, pages: Optional[LaPages], q, k, v, g, beta, cu_dev, cu_host, start_dev,
+                     start_host, o, final_state, ckpt_off_dev, ckpt_off_host, workspace, stream=None,
+                     check: bool = True) -> int:
+    """A prefill whose checkpoints go to pool pages and whose starting states
+    come from pool pages; start_dev / start_host None make it a cold call."""
+    cu_host = np.ascontiguousarray(cu_host, dtype=np.int32)
+    sh = None if start_host is None else np.ascontiguousarray(start_host, dtype=np.int64)
+    oh = None if ckpt_off_host is None else np.ascontiguousarray(ckpt_off_host, dtype=np.int32)
+    st = _lib.la_prefill_paged(ctypes.byref(shape), None if pages is None else ctypes.byref(pages), _dptr(q),
+                               _dptr(k), _dptr(v), _dptr(g), _dptr(beta), _dptr(cu_dev), _hptr(cu_host, np.int32),
+                               _dptr(start_dev), _hptr(sh, np.int64), _dptr(o), _dptr(final_state),
+                               _dptr(ckpt_off_dev), _hptr(oh, np.int32), _dptr(workspace),
+                               workspace.numel() * workspace.element_size(), _stream(stream))
     if check:
         _check(st)
     return st

@@ -153,6 +153,33 @@ def test_stage_mask_validation_before_launch():
     assert call(la.LA_STAGE_SCAN, state_in=FAKE, starts=[8]) == la.LA_ERR_MISALIGNED_STATE
 
 
+def test_paged_prefill_validation_before_launch():
+    lib = la.library()
+    sh = la.make_shape(1, 1, 64, 64, 16)
+    cu = np.array([0, 64], np.int32)
+    offs = np.array([0], np.int32)
+    P = la.ctypes.c_void_p
+    ws = lib.la_prefill_workspace_bytes(la.ctypes.byref(sh), 64)
+
+    def call(pool=FAKE, ck=None, st_ids=None, starts=None, offsets=True, n_pages=4, null_pages=False):
+        pg = la.LaPages(pool, n_pages, ck, st_ids, None)
+        st = None if starts is None else np.asarray(starts, np.int64)
+        return lib.la_prefill_paged(la.ctypes.byref(sh), None if null_pages else la.ctypes.byref(pg),
+                                    FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, P(cu.ctypes.data),
+                                    FAKE if st is not None else None, P(st.ctypes.data) if st is not None else None,
+                                    FAKE, FAKE, FAKE if offsets else None, P(offs.ctypes.data) if offsets else None,
+                                    FAKE, ws, None)
+    assert call(null_pages=True) == la.LA_ERR_INVALID_ARG
+    assert call(st_ids=FAKE) == la.LA_ERR_INVALID_ARG                     # starting pages, cold call
+    assert call(starts=[16]) == la.LA_ERR_INVALID_ARG                      # resume without starting pages
+    assert call(pool=None, ck=FAKE) == la.LA_ERR_INVALID_ARG               # page ids without a pool
+    assert call(pool=FAKE + 4, ck=FAKE) == la.LA_ERR_INVALID_ARG           # misaligned pool
+    assert call(ck=FAKE, offsets=False) == la.LA_ERR_INVALID_ARG           # checkpoint pages need row offsets
+    assert call(ck=FAKE, n_pages=-1) == la.LA_ERR_INVALID_ARG
+    assert call(ck=FAKE, n_pages=1 << 31) == la.LA_ERR_INVALID_ARG
+    assert call(st_ids=FAKE, starts=[8]) == la.LA_ERR_MISALIGNED_STATE
+
+
 def test_decode_validation_before_launch():
     lib = la.library()
     sh = la.make_shape(2, 8, 128, 128, 256)
