@@ -7,7 +7,9 @@
 //   Gp_r  = G_{r-1} (literal rule; G_{-1} = 0) or G_r (decayed rule)
 //   A     = strictly lower part of beta_r exp(Gp_r - G_s) (k_r . k_s)
 //   X     = (I + A)^{-1}                       (unit lower triangular, fp32)
-//   W     = X diag(beta exp(Gp)) K             (stored negated, A-operand order)
+//   W     = X diag(beta exp(Gp)) K             (stored negated, A-operand order;
+//                                               computed as W^T tiles, whose
+//                                               accumulator layout is that order)
 //   U~    = X diag(beta) V                     (fp32, C-layout)
 //   K~^T  = (diag(exp(G_63 - G)) K)^T          (A-operand order, chunk rows permuted)
 //   P     = (Q K^T) exp(G_r - G_s) on s <= r   (for the output; B operand of P^T
@@ -42,7 +44,7 @@ template <typename T, int DK, int DV> struct alignas(16) PrepSmem {
     static constexpr int PK = Vec<T>::N;       // row pads keep 16-byte alignment
     static constexpr int DM = DK > DV ? DK : DV;
     T ks[kChunk][DK + PK];                     // K, row-major
-    T vs[kChunk][DM + PK];                     // V, row-major; later -W staging
+    T vs[kChunk][DM + PK];                     // V, row-major
     float am[kChunk][kChunk + 4];              // A (strictly lower)
     float xm[kChunk][kChunk + 4];              // X = (I + A)^{-1}
     float ysc[4][16][17];                      // per-wave 16x16 scratch
@@ -211,35 +213,36 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
     __syncthreads();
 
     // ---- 3. A = strictly-lower beta_r exp(Gp_r - G_s) K K^T ------------------
-    // The 10 lower 16x16 tiles (row-major over the lower triangle, diagonal
-    // included) are dealt 3/3/2/2 over the waves.  A tile's row tile is a
-    // run-time value, so its gate and beta values are read from LDS per tile
-    // (a register array indexed by it would become a select chain), and its
-    // coordinates are computed, not looked up (a table indexed at run time
-    // would live in scratch memory).
+    // Wave w computes row tile w against all four column tiles: four
+    // independent MFMA chains with no branch between them (the tiles above
+    // the diagonal are computed and dropped: they are never read).  The row
+    // tile's K fragments are read once and reused for every column tile.
     {
+        const int mt = wave;
+        typename M::frag ka[DK / KSTEP];
 #pragma unroll
-        for (int q = 0; q < 3; ++q) {
-            const int t = wave + 4 * q;
-            if (t < 10) {
-                const int mt = t >= 6 ? 3 : t >= 3 ? 2 : t >= 1 ? 1 : 0;
-                const int nt = t - mt * (mt + 1) / 2;
-                const float4 brow = *(const float4 *)&sm.bs[16 * mt + 4 * g16];
-                const float4 gprow = *(const float4 *)&sm.Gp2[16 * mt + 4 * g16];
-                const float gcol = sm.G2[16 * nt + c16];
-                f32x4 acc = zero4();
+        for (int ks = 0; ks < DK / KSTEP; ++ks) ka[ks] = M::pack(&sm.ks[16 * mt + c16][ks * KSTEP + g16 * KW]);
+        f32x4 acc[4];
 #pragma unroll
-                for (int ks = 0; ks < DK / KSTEP; ++ks)
-                    acc = M::mma(M::pack(&sm.ks[16 * mt + c16][ks * KSTEP + g16 * KW]),
-                                 M::pack(&sm.ks[16 * nt + c16][ks * KSTEP + g16 * KW]), acc);
-                const float bv[4] = {brow.x, brow.y, brow.z, brow.w};
-                const float gv[4] = {gprow.x, gprow.y, gprow.z, gprow.w};
+        for (int nt = 0; nt < 4; ++nt) {
+            acc[nt] = zero4();
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int r = 16 * mt + 4 * g16 + i, s = 16 * nt + c16;
-                    const float e = __builtin_amdgcn_exp2f(gv[i] - gcol);
-                    sm.am[r][s] = (s < r) ? bv[i] * e * acc[i] : 0.f;
-                }
+            for (int ks = 0; ks < DK / KSTEP; ++ks)
+                acc[nt] = M::mma(ka[ks], M::pack(&sm.ks[16 * nt + c16][ks * KSTEP + g16 * KW]), acc[nt]);
+        }
+        const float4 brow = *(const float4 *)&sm.bs[16 * mt + 4 * g16];
+        const float4 gprow = *(const float4 *)&sm.Gp2[16 * mt + 4 * g16];
+        const float bv[4] = {brow.x, brow.y, brow.z, brow.w};
+        const float gv[4] = {gprow.x, gprow.y, gprow.z, gprow.w};
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            if (nt > mt) continue;   // wave-uniform
+            const float gcol = sm.G2[16 * nt + c16];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = 16 * mt + 4 * g16 + i, s = 16 * nt + c16;
+                const float e = __builtin_amdgcn_exp2f(gv[i] - gcol);
+                sm.am[r][s] = (s < r) ? bv[i] * e * acc[nt][i] : 0.f;
             }
         }
     }
@@ -296,8 +299,7 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
         __syncthreads();
     }
 
-    // ---- 5. W = X diag(dW) K, U~ = X diag(beta) V, K~^T fragments -------------
-    f32x4 wt[DK / 16];
+    // ---- 5. W, U~ = X diag(beta) V, K~^T, P and Q fragments --------------------
     {
         const int mt = wave;
         constexpr int NKS = kChunk / KSTEP;
@@ -315,13 +317,28 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
             f1[ks] = M::pack(v1);
             f2[ks] = M::pack(v2);
         }
+        // W^T tile (dk tile nt, row tile mt) = K^T (X diag(dW))^T: per lane the
+        // K fragment read as a B operand of K is the A operand of K^T, and f1
+        // (A operand of X diag(dW)) is the B operand of its transpose.  The
+        // accumulator then holds W[16 mt + c16][16 nt + 4 g + i], element
+        // 4 nt + i of this lane's -W fragment in the scan's permuted dk
+        // order, so -W is stored straight from registers.
+        {
+            T wf[DK / 4];
 #pragma unroll
-        for (int nt = 0; nt < DK / 16; ++nt) {
-            f32x4 acc = zero4();
+            for (int nt = 0; nt < DK / 16; ++nt) {
+                f32x4 acc = zero4();
 #pragma unroll
-            for (int ks = 0; ks < NKS; ++ks)
-                acc = M::mma(f1[ks], RT::bfrag(&sm.ks[0][0], LDK, ks * KSTEP, 16 * nt, lane), acc);
-            wt[nt] = acc;
+                for (int ks = 0; ks < NKS; ++ks)
+                    acc = M::mma(RT::bfrag(&sm.ks[0][0], LDK, ks * KSTEP, 16 * nt, lane), f1[ks], acc);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) wf[4 * nt + i] = from_f32<T>(-acc[i]);
+            }
+            constexpr int NV = DK / 4 / VEC;
+            T *wout = (T *)a.ws.w + sh * WsLayout<T, DK, DV>::w_elems;
+#pragma unroll
+            for (int v = 0; v < NV; ++v)
+                *(uint4 *)(wout + ((size_t)(mt * NV + v) * 64 + lane) * VEC) = *(const uint4 *)&wf[v * VEC];
         }
         float4 *ut = (float4 *)(a.ws.ut + sh * WsLayout<T, DK, DV>::ut_elems);
 #pragma unroll
@@ -389,30 +406,6 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
 #pragma unroll
             for (int v = 0; v < NQ; ++v)
                 *(uint4 *)(qout + ((size_t)(mt * NQ + v) * 64 + lane) * VEC) = *(const uint4 *)&qf[v * VEC];
-        }
-    }
-    __syncthreads();   // every wave is done reading ks and vs
-    {
-        const int mt = wave;
-#pragma unroll
-        for (int nt = 0; nt < DK / 16; ++nt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                sm.vs[16 * mt + 4 * g16 + i][16 * nt + c16] = from_f32<T>(-wt[nt][i]);
-    }
-    __syncthreads();
-
-    // ---- 6. write -W in A-operand order (columns perm_row(f, g)) ---------------
-    {
-        constexpr int NV = DK / 4 / VEC;
-        T *wout = (T *)a.ws.w + sh * WsLayout<T, DK, DV>::w_elems;
-        for (int vi = tid; vi < 4 * NV * 64; vi += 256) {
-            const int ln = vi & 63, v = (vi >> 6) % NV, mt = vi / (64 * NV);
-            const int r = 16 * mt + (ln & 15), g = ln >> 4;
-            T buf[VEC];
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) buf[e] = sm.vs[r][perm_row(v * VEC + e, g)];
-            *(uint4 *)(wout + (size_t)vi * VEC) = *(const uint4 *)buf;
         }
     }
 }
