@@ -15,7 +15,9 @@ Contents
   rules by brute-force enumeration (``boundary.py``).
 * ``paged_save`` / ``paged_restore``: the state pool as NumPy fancy
   indexing (``paging.py``).
+* ``hybrid_boundary`` / ``hybrid_restore``: the joint attention-KV and
+  recurrent-state boundary, by enumeration, and its restore as plain loops.
 """
 from .gdr import gdr_prefill, gdr_prefill_seq, build_oracle, oracle_library_path  # noqa: F401
-from .boundary import strict_prefix_boundary, nonstrict_lookup  # noqa: F401
-from .paging import paged_save, paged_restore  # noqa: F401
+from .boundary import strict_prefix_boundary, nonstrict_lookup, hybrid_boundary  # noqa: F401
+from .paging import paged_save, paged_restore, hybrid_restore  # noqa: F401

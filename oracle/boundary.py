@@ -53,3 +53,30 @@ def nonstrict_lookup(n_tokens: int, interval: int, available: int):
         b += interval
     p = n_tokens - 1 if best == n_tokens else best
     return best, p
+
+
+def hybrid_boundary(n_tokens: int, interval: int, kv_block_tokens: int, kv_cached: int, state_cached: int):
+    """Joint boundary of a hybrid cache: attention KV blocks and recurrent
+    checkpoints restored at one position B (sections 1 and 6: reusable
+    attention prefixes must align with recurrent checkpoints).
+
+    B is the largest b = j * C with b <= N - 1 (the strict prefix of section
+    2.2) whose every KV block [0, b) is cached (the first kv_cached tokens
+    are, in whole blocks of kv_block_tokens) and whose checkpoint exists
+    (checkpoints are cached for every multiple of C up to state_cached).
+    Returns (B, number of KV blocks in [0, B)).  Raises ValueError when the
+    blocks do not tile the checkpoint interval (no checkpoint position would
+    fall on a block boundary) or on negative or zero sizes.
+    """
+    if n_tokens < 1 or interval < 1 or kv_block_tokens < 1 or kv_cached < 0 or state_cached < 0:
+        raise ValueError("hybrid_boundary needs N, C, block >= 1 and cached lengths >= 0")
+    if interval % kv_block_tokens != 0:
+        raise ValueError("KV blocks must tile the checkpoint interval")
+    best = 0
+    b = 0
+    while b <= n_tokens - 1:
+        blocks_cached = all((j + 1) * kv_block_tokens <= kv_cached for j in range(b // kv_block_tokens))
+        if blocks_cached and b <= state_cached:
+            best = b
+        b += interval
+    return best, best // kv_block_tokens
