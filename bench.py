@@ -16,9 +16,12 @@ checkpoint interval C = 256):
 
 Beside the step it reports, each on its own timer: paged save/restore
 bandwidth on the full 4,096-page pool, decode continuation (one token per
-sequence and head per call, state in HBM) at 1 and 64 sequences, and the
+sequence and head per call, state in HBM) at 1 and 64 sequences, the
 host-memory tier (pages to and from a pinned host pool) for the 112
-checkpoint pages of a step and for 4,096 pages.
+checkpoint pages of a step and for 4,096 pages, and the joint restore of a
+hybrid cache at the reload's boundary (the attention KV blocks of [0, B),
+8,268 B per token per rank, with the state pages at B) from a device and
+from a pinned host pool.
 
 Inputs are resident in HBM before timing starts.  The JSON line reports
 whole-step prefill tokens/s (3,584 + 256 tokens per step), the dominant
@@ -206,6 +209,56 @@ def bench_host_tier(la, torch, stream_ptr, events, sizes=(112, 4096), page_elems
     return out
 
 
+KV_TOKEN_BYTES = 8268    # attention entries per token per rank, fixed by the paper's reload byte counts
+KV_BLOCK_TOKENS = 16
+
+
+def bench_hybrid(la, torch, stream_ptr, events, n_tokens, interval, n_heads, page_elems=128 * 128, reps=20):
+    """Joint restore at the one-TP-rank reload: the attention KV blocks of the
+    prefix [0, B) (opaque bytes, 8,268 per token) and the 8 state pages of the
+    checkpoint at B, in one launch, from a device pool and from a pinned
+    host pool.  Payload GB/s over back-to-back launches; the device-pool
+    figure also as HBM traffic (read + write) against the HBM peak."""
+    B, nb = la.la_hybrid_boundary(n_tokens, interval, KV_BLOCK_TOKENS, n_tokens, n_tokens)
+    block = KV_TOKEN_BYTES * KV_BLOCK_TOKENS
+    rng = np.random.default_rng(9)
+    n_blocks = n_tokens // KV_BLOCK_TOKENS
+    kv_dev = torch.randint(0, 256, (n_blocks, block), dtype=torch.uint8, device="cuda")
+    kv_host = torch.empty((n_blocks, block), dtype=torch.uint8, pin_memory=True)
+    kv_host.copy_(kv_dev)
+    n_pages = 14 * n_heads
+    st_dev = torch.randn((n_pages, page_elems), device="cuda")
+    st_host = torch.empty((n_pages, page_elems), dtype=torch.float32, pin_memory=True)
+    st_host.copy_(st_dev)
+    cache = torch.empty((nb + 16, block), dtype=torch.uint8, device="cuda")
+    src = torch.from_numpy(rng.permutation(n_blocks)[:nb].astype(np.int32)[None]).cuda()
+    dst = torch.from_numpy(rng.permutation(nb + 16)[:nb].astype(np.int32)[None]).cuda()
+    sid = torch.from_numpy(rng.permutation(n_pages)[:n_heads].astype(np.int32)).cuda()
+    states = torch.empty((n_heads, page_elems), device="cuda")
+    bdev = torch.tensor([B], dtype=torch.int64, device="cuda")
+    payload = nb * block + n_heads * page_elems * 4
+    out = {"boundary": B, "kv_blocks": nb, "kv_block_bytes": block, "payload_bytes": payload}
+    for name, kvp, stp in (("device_pool", kv_dev, st_dev), ("host_pool", kv_host, st_host)):
+        kv = la.make_kv_blocks(kvp, cache, src, dst, KV_BLOCK_TOKENS)
+        for _ in range(3):
+            la.la_hybrid_restore(kv, bdev, [B], stp, sid, states, n_heads)
+        torch.cuda.synchronize()
+        # back-to-back launches: the entry point's host-side checks of the pools
+        # overlap the previous launch instead of idling the GPU between events
+        events.record(4, stream_ptr)
+        for _ in range(reps):
+            la.la_hybrid_restore(kv, bdev, [B], stp, sid, states, n_heads)
+        events.record(5, stream_ptr)
+        us = events.ms(4, 5) / reps * 1e3
+        gbps = payload / (us * 1e-6) / 1e9
+        out[name] = {"us": round(us, 2), "payload_GBps": round(gbps, 1)}
+        if name == "device_pool":
+            out[name]["hbm_frac"] = round(2 * gbps / HBM_PEAK_GBPS, 4)
+    got = cache[dst[0].long()].cpu()
+    assert torch.equal(got, kv_dev[src[0].long()].cpu()) and torch.equal(states, st_dev[sid.long()])
+    return out
+
+
 def bench_pool(la, torch, stream_ptr, events, n_pages=4096, page_elems=128 * 128, reps=20):
     """Full-pool scatter and gather under a random permutation (2 x 256 MiB)."""
     rng = np.random.default_rng(7)
@@ -358,6 +411,7 @@ def main():
     out["decode"] = bench_decode(la, torch, sp, ev, H, dk, dv, C)
     if not args.no_pool:
         out["host_tier"] = bench_host_tier(la, torch, sp, ev)
+        out["hybrid_restore"] = bench_hybrid(la, torch, sp, ev, N, C, H)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, B, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -285,6 +285,71 @@ la_status la_state_restore_paged(const float *pool, int64_t n_pages,
                                  int32_t *err_count_dev, void *stream);
 
 /*
+ * la_hybrid_boundary - the position a hybrid cache resumes from: attention
+ * KV blocks and recurrent checkpoints restored together at one B.  A reload
+ * moves both kinds of entries (section 2.1; Table 5), and the attention
+ * prefix must end where the checkpoint's prefix ends (sections 1 and 6).
+ *
+ * B is the strict-prefix boundary (section 2.2) over the shorter of the two
+ * cached prefixes: the largest multiple of C with B <= N - 1, B <=
+ * kv_cached_tokens (the first KV blocks, of kv_block_tokens tokens each,
+ * that are cached contiguously) and B <= state_cached_tokens (checkpoints
+ * exist at every multiple of C up to it).  *kv_blocks_out = B /
+ * kv_block_tokens, the blocks that cover [0, B).  Errors: INVALID_ARG for
+ * N < 1, C < 1, kv_block_tokens < 1, negative cached lengths or NULL
+ * outputs; MISALIGNED_STATE when kv_block_tokens does not divide C (no
+ * checkpoint position falls on a block boundary).
+ */
+la_status la_hybrid_boundary(int64_t n_tokens, int64_t interval, int64_t kv_block_tokens,
+                             int64_t kv_cached_tokens, int64_t state_cached_tokens,
+                             int64_t *boundary_out, int64_t *kv_blocks_out);
+
+/*
+ * la_hybrid_restore - restore, in one launch, every sequence's attention KV
+ * blocks of the prefix [0, B_i) and its recurrent state pages of the
+ * checkpoint at B_i (the joint reload of section 2.1 and Table 5, at the
+ * boundary la_hybrid_boundary gives).
+ *
+ * kv: the attention KV pages of this rank, opaque bytes.
+ *   pool     [n_pool_blocks, block_bytes]: device memory, or pinned host
+ *            memory mapped into the device (the CPU tier of section 2.1).
+ *   cache    [n_cache_blocks, block_bytes] device: the engine's KV cache.
+ *   src_ids, dst_ids  device int32 [n_seqs, max_blocks]: block j < B_i /
+ *            block_tokens of sequence i goes from pool[src_ids[i][j]] to
+ *            cache[dst_ids[i][j]]; either id -1 skips it, ids out of range
+ *            skip it and count.  block_bytes a positive multiple of 16.
+ * boundary_dev/host  int64 [n_seqs]: B_i, a multiple of block_tokens with
+ *            B_i / block_tokens <= max_blocks (MISALIGNED_STATE / INVALID_ARG
+ *            before any launch otherwise).
+ * State pages (page_elems fp32 each, one head's state, as la_state_restore_paged):
+ *   state_pool [n_state_pages, page_elems]: device or pinned host memory;
+ *   state_page_ids_dev int32 [n_seqs * n_heads]; states [n_seqs * n_heads,
+ *   page_elems] device: id -1 writes the zero state, ids out of range leave
+ *   the item untouched and count.  n_heads = 0 restores no state.
+ * err_count_dev (device int32, may be NULL) counts every out-of-range id.
+ * Pools given as pinned host memory are checked with
+ * hipPointerGetAttributes before any launch (pageable memory: INVALID_ARG).
+ * The caller owns every buffer; cache and states must not alias the pools.
+ */
+typedef struct {
+    const void *pool;
+    int64_t n_pool_blocks;
+    void *cache;
+    int64_t n_cache_blocks;
+    int64_t block_bytes;
+    int64_t block_tokens;
+    const int32_t *src_ids;
+    const int32_t *dst_ids;
+    int64_t max_blocks;
+} la_kv_blocks;
+
+la_status la_hybrid_restore(const la_kv_blocks *kv, int32_t n_seqs, int32_t n_heads, int64_t page_elems,
+                            const int64_t *boundary_dev, const int64_t *boundary_host,
+                            const float *state_pool, int64_t n_state_pages,
+                            const int32_t *state_page_ids_dev, float *states,
+                            int32_t *err_count_dev, void *stream);
+
+/*
  * la_state_save_host / la_state_restore_host - the host-memory tier: the
  * same page scatter and gather as la_state_save_paged / la_state_restore_paged
  * with the pool in pinned host memory (the paper's CPU reload path, section

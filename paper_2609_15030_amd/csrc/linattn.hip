@@ -18,6 +18,7 @@
 #include "gdr_out.h"
 #include "gdr_decode.h"
 #include "paged.h"
+#include "hybrid.h"
 
 namespace {
 
@@ -430,6 +431,29 @@ la_status host_pool_device_ptr(const float *pool, size_t bytes, float **dev) {
     return LA_OK;
 }
 
+// A pool the kernels read directly: device memory as is, or pinned host
+// memory through its device mapping (checked at both ends).  Pageable or
+// unknown memory is refused.
+la_status resolve_pool(const void *p, size_t bytes, const void **dev, const char *what) {
+    *dev = nullptr;
+    hipPointerAttribute_t at{};
+    if (!p || hipPointerGetAttributes(&at, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(LA_ERR_INVALID_ARG, "%s is neither device memory nor pinned, device-mapped host memory", what);
+    }
+    if (at.type == hipMemoryTypeDevice) {
+        *dev = p;
+        return LA_OK;
+    }
+    if (at.type == hipMemoryTypeHost) {
+        float *d = nullptr;
+        if (la_status e = host_pool_device_ptr((const float *)p, bytes, &d)) return e;
+        *dev = d;
+        return LA_OK;
+    }
+    return fail(LA_ERR_INVALID_ARG, "%s is neither device memory nor pinned, device-mapped host memory", what);
+}
+
 la_status record_done(void *done_event, void *stream) {
     if (done_event && hipEventRecord((hipEvent_t)done_event, (hipStream_t)stream) != hipSuccess)
         return hip_check("completion event record");
@@ -461,6 +485,106 @@ la_status strict_prefix_boundary(int64_t n_tokens, int64_t interval, int64_t ava
     const int64_t avail = available_tokens / interval * interval;    // only whole cached blocks
     *boundary_out = std::min(query, avail);
     return LA_OK;
+}
+
+la_status la_hybrid_boundary(int64_t n_tokens, int64_t interval, int64_t kv_block_tokens, int64_t kv_cached_tokens,
+                             int64_t state_cached_tokens, int64_t *boundary_out, int64_t *kv_blocks_out) {
+    if (!boundary_out || !kv_blocks_out) return fail(LA_ERR_INVALID_ARG, "boundary_out and kv_blocks_out are required");
+    if (kv_block_tokens < 1) return fail(LA_ERR_INVALID_ARG, "kv_block_tokens=%lld < 1", (long long)kv_block_tokens);
+    if (kv_cached_tokens < 0 || state_cached_tokens < 0)
+        return fail(LA_ERR_INVALID_ARG, "cached lengths must be >= 0");
+    if (interval >= 1 && interval % kv_block_tokens != 0)
+        return fail(LA_ERR_MISALIGNED_STATE, "KV blocks of %lld tokens do not tile the checkpoint interval C=%lld",
+                    (long long)kv_block_tokens, (long long)interval);
+    int64_t b = 0;
+    if (la_status e = strict_prefix_boundary(n_tokens, interval, std::min(kv_cached_tokens, state_cached_tokens), &b))
+        return e;
+    *boundary_out = b;
+    *kv_blocks_out = b / kv_block_tokens;
+    return LA_OK;
+}
+
+la_status la_hybrid_restore(const la_kv_blocks *kv, int32_t n_seqs, int32_t n_heads, int64_t page_elems,
+                            const int64_t *boundary_dev, const int64_t *boundary_host, const float *state_pool,
+                            int64_t n_state_pages, const int32_t *state_page_ids_dev, float *states,
+                            int32_t *err_count_dev, void *stream) {
+    if (!kv) return fail(LA_ERR_INVALID_ARG, "kv is NULL");
+    if (n_seqs < 0 || n_seqs > 65535) return fail(LA_ERR_INVALID_ARG, "n_seqs=%d outside [0, 65535]", n_seqs);
+    if (n_heads < 0 || n_heads > 65535) return fail(LA_ERR_INVALID_ARG, "n_heads=%d outside [0, 65535]", n_heads);
+    if (kv->block_tokens < 1) return fail(LA_ERR_INVALID_ARG, "block_tokens=%lld < 1", (long long)kv->block_tokens);
+    if (kv->block_bytes <= 0 || kv->block_bytes % 16 != 0)
+        return fail(LA_ERR_INVALID_ARG, "block_bytes=%lld must be a positive multiple of 16", (long long)kv->block_bytes);
+    if (kv->max_blocks < 0 || kv->max_blocks > 0x7fffffff || kv->n_pool_blocks < 0 || kv->n_pool_blocks > 0x7fffffff ||
+        kv->n_cache_blocks < 0 || kv->n_cache_blocks > 0x7fffffff)
+        return fail(LA_ERR_INVALID_ARG, "block counts outside [0, 2^31)");
+    if (n_seqs == 0) return LA_OK;
+    if (!boundary_dev || !boundary_host) return fail(LA_ERR_INVALID_ARG, "boundary_dev and boundary_host are required");
+    int64_t nb_max = 0;
+    for (int i = 0; i < n_seqs; ++i) {
+        const int64_t b = boundary_host[i];
+        if (b < 0) return fail(LA_ERR_INVALID_ARG, "boundary[%d]=%lld < 0", i, (long long)b);
+        if (b % kv->block_tokens != 0)
+            return fail(LA_ERR_MISALIGNED_STATE, "boundary[%d]=%lld is not a multiple of the KV block (%lld tokens)", i,
+                        (long long)b, (long long)kv->block_tokens);
+        if (b / kv->block_tokens > kv->max_blocks)
+            return fail(LA_ERR_INVALID_ARG, "boundary[%d] needs %lld blocks, max_blocks=%lld", i,
+                        (long long)(b / kv->block_tokens), (long long)kv->max_blocks);
+        nb_max = std::max(nb_max, b / kv->block_tokens);
+    }
+    if (nb_max + n_heads > 0x7fffffff) return fail(LA_ERR_INVALID_ARG, "too many blocks for one launch");
+    const void *kv_pool = nullptr;
+    if (nb_max > 0) {
+        if (!kv->cache || !kv->src_ids || !kv->dst_ids)
+            return fail(LA_ERR_INVALID_ARG, "kv cache, src_ids and dst_ids are required");
+        if (!aligned16(kv->cache)) return fail(LA_ERR_INVALID_ARG, "kv cache must be 16-byte aligned");
+        if (kv->n_pool_blocks > 0) {
+            if (la_status e = resolve_pool(kv->pool, (size_t)kv->n_pool_blocks * kv->block_bytes, &kv_pool, "kv pool"))
+                return e;
+            if (!aligned16(kv_pool)) return fail(LA_ERR_INVALID_ARG, "kv pool must be 16-byte aligned");
+        }
+    }
+    const void *st_pool = nullptr;
+    if (n_heads > 0) {
+        if (page_elems <= 0 || page_elems % 4 != 0)
+            return fail(LA_ERR_INVALID_ARG, "page_elems=%lld must be a positive multiple of 4", (long long)page_elems);
+        if (n_state_pages < 0 || n_state_pages > 0x7fffffff)
+            return fail(LA_ERR_INVALID_ARG, "n_state_pages=%lld", (long long)n_state_pages);
+        if (!state_page_ids_dev || !states) return fail(LA_ERR_INVALID_ARG, "state_page_ids and states are required");
+        if (!aligned16(states)) return fail(LA_ERR_INVALID_ARG, "states must be 16-byte aligned");
+        if (n_state_pages > 0) {
+            if (la_status e = resolve_pool(state_pool, (size_t)n_state_pages * page_elems * sizeof(float), &st_pool,
+                                           "state pool"))
+                return e;
+            if (!aligned16(st_pool)) return fail(LA_ERR_INVALID_ARG, "state pool must be 16-byte aligned");
+        }
+    }
+    if (nb_max + n_heads == 0) return LA_OK;
+    la::HybridArgs a{};
+    a.kv_pool = (const la::f32x4 *)kv_pool;
+    a.cache = (la::f32x4 *)kv->cache;
+    a.src_ids = kv->src_ids;
+    a.dst_ids = kv->dst_ids;
+    a.boundary = boundary_dev;
+    a.state_pool = (const la::f32x4 *)st_pool;
+    a.state_ids = state_page_ids_dev;
+    a.states = (la::f32x4 *)states;
+    a.err = err_count_dev;
+    a.kv_vec = kv->block_bytes / 16;
+    a.n_pool_blocks = kv->n_pool_blocks;
+    a.n_cache_blocks = kv->n_cache_blocks;
+    a.max_blocks = kv->max_blocks;
+    a.block_tokens = kv->block_tokens;
+    a.page_vec = n_heads > 0 ? page_elems / 4 : 0;
+    a.n_state_pages = n_heads > 0 ? n_state_pages : 0;
+    a.n_heads = n_heads;
+    a.nb_max = (int32_t)nb_max;
+    const int64_t parts = (std::max(nb_max > 0 ? a.kv_vec : 0, a.page_vec) + la::kHybridPartVec - 1) /
+                          la::kHybridPartVec;
+    if (parts > 65535) return fail(LA_ERR_INVALID_ARG, "blocks or pages too large for one launch");
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(la::hybrid_restore_kernel, dim3((unsigned)(nb_max + n_heads), (unsigned)n_seqs, (unsigned)parts),
+                       dim3(la::kPageThreads), 0, (hipStream_t)stream, a);
+    return hip_check("hybrid restore launch");
 }
 
 size_t la_prefill_workspace_bytes(const la_shape *shape, int64_t total_tokens) {

@@ -34,7 +34,7 @@ LA_GDR_DECAYED_DELTA = 1
 EXPORTED = ("strict_prefix_boundary", "la_prefill_workspace_bytes", "la_prefill",
             "la_prefill_resume", "la_prefill_stages", "la_prefill_paged", "la_decode_step", "la_state_save_paged",
             "la_state_restore_paged",
-            "la_state_save_host", "la_state_restore_host",
+            "la_state_save_host", "la_state_restore_host", "la_hybrid_boundary", "la_hybrid_restore",
             "la_status_string", "la_last_error_message", "la_trace_set_events")
 
 
@@ -50,6 +50,13 @@ class LaPages(ctypes.Structure):
     _fields_ = [("pool", ctypes.c_void_p), ("n_pages", ctypes.c_int64),
                 ("ckpt_page_ids", ctypes.c_void_p), ("state_page_ids", ctypes.c_void_p),
                 ("err_count", ctypes.c_void_p)]
+
+
+class LaKvBlocks(ctypes.Structure):
+    _fields_ = [("pool", ctypes.c_void_p), ("n_pool_blocks", ctypes.c_int64),
+                ("cache", ctypes.c_void_p), ("n_cache_blocks", ctypes.c_int64),
+                ("block_bytes", ctypes.c_int64), ("block_tokens", ctypes.c_int64),
+                ("src_ids", ctypes.c_void_p), ("dst_ids", ctypes.c_void_p), ("max_blocks", ctypes.c_int64)]
 
 
 def make_shape(n_seqs, n_heads, dk, dv, ckpt_interval, io_dtype=LA_BF16,
@@ -87,6 +94,8 @@ def _load() -> ctypes.CDLL:
         "la_state_restore_paged": ([P, I64, P, P, I64, I64, P, P], I32),
         "la_state_save_host": ([P, I64, I64, P, I64, P, P, P, P], I32),
         "la_state_restore_host": ([P, I64, P, P, I64, I64, P, P, P], I32),
+        "la_hybrid_boundary": ([I64, I64, I64, I64, I64, ctypes.POINTER(I64), ctypes.POINTER(I64)], I32),
+        "la_hybrid_restore": ([ctypes.POINTER(LaKvBlocks), I32, I32, I64, P, P, P, I64, P, P, P, P], I32),
         "la_status_string": ([I32], ctypes.c_char_p),
         "la_last_error_message": ([], ctypes.c_char_p),
         "la_trace_set_events": ([ctypes.POINTER(P), I32], None),
@@ -249,7 +258,9 @@ def la_prefill_stages(shape: LaShape, stages: int, q, k, v, g, beta, cu_dev, cu_
 def make_pages(pool, ckpt_page_ids=None, state_page_ids=None, err_count=None, n_pages=None) -> LaPages:
     """la_pages for a device pool ([n_pages, dk * dv] fp32) and device int32 page tables."""
     n = pool.shape[0] if n_pages is None else n_pages
-    return LaPages(_dptr(pool), int(n), _dptr(ckpt_page_ids), _dptr(state_page_ids), _dptr(err_count))
+    pages = LaPages(_dptr(pool), int(n), _dptr(ckpt_page_ids), _dptr(state_page_ids), _dptr(err_count))
+    pages._keep = (pool, ckpt_page_ids, state_page_ids, err_count)   # the struct holds raw addresses only
+    return pages
 
 
 def la_prefill_paged(shape: LaShape, pages: Optional[LaPages], q, k, v, g, beta, cu_dev, cu_host, start_dev,
@@ -310,6 +321,50 @@ def la_state_restore_host(host_pool, page_ids_dev, states, err_count_dev=None, s
     n_items = page_ids_dev.numel()
     st = _lib.la_state_restore_host(_hostptr(host_pool), n_pages, _dptr(page_ids_dev), _dptr(states), n_items,
                                     page_elems, _dptr(err_count_dev), _stream(stream), done_event)
+    if check:
+        _check(st)
+    return st
+
+
+def la_hybrid_boundary(n_tokens: int, interval: int, kv_block_tokens: int, kv_cached_tokens: int,
+                       state_cached_tokens: int):
+    """(B, KV blocks covering [0, B)) for a hybrid cache."""
+    b, nb = ctypes.c_int64(-1), ctypes.c_int64(-1)
+    _check(_lib.la_hybrid_boundary(int(n_tokens), int(interval), int(kv_block_tokens), int(kv_cached_tokens),
+                                   int(state_cached_tokens), ctypes.byref(b), ctypes.byref(nb)))
+    return b.value, nb.value
+
+
+def _anyptr(t) -> Optional[int]:
+    """Address of a device tensor or of a pinned host tensor (the library checks which)."""
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def make_kv_blocks(pool, cache, src_ids, dst_ids, block_tokens: int) -> LaKvBlocks:
+    """la_kv_blocks for byte pools [n_blocks, block_bytes] (uint8 tensors; the pool
+    may be pinned host memory) and device int32 tables [n_seqs, max_blocks]."""
+    kv = LaKvBlocks(_anyptr(pool), int(pool.shape[0]), _dptr(cache), int(cache.shape[0]),
+                    int(cache.shape[1] if cache.dim() > 1 else pool.shape[1]), int(block_tokens),
+                    _dptr(src_ids), _dptr(dst_ids), int(src_ids.shape[1]))
+    kv._keep = (pool, cache, src_ids, dst_ids)     # the struct holds raw addresses only
+    return kv
+
+
+def la_hybrid_restore(kv: LaKvBlocks, boundary_dev, boundary_host, state_pool, state_page_ids_dev, states,
+                      n_heads: int, err_count_dev=None, stream=None, check: bool = True) -> int:
+    """Joint restore: KV blocks of every prefix [0, B_i) and the state pages of the
+    checkpoint at B_i.  states: [n_seqs * n_heads, page_elems] device fp32."""
+    bh = np.ascontiguousarray(boundary_host, dtype=np.int64)
+    n_seqs = len(bh)
+    page_elems = states.shape[-1] if states is not None else 0
+    n_state_pages = state_pool.shape[0] if state_pool is not None else 0
+    st = _lib.la_hybrid_restore(ctypes.byref(kv), n_seqs, int(n_heads), int(page_elems), _dptr(boundary_dev),
+                                _hptr(bh, np.int64), _anyptr(state_pool), int(n_state_pages),
+                                _dptr(state_page_ids_dev), _dptr(states), _dptr(err_count_dev), _stream(stream))
     if check:
         _check(st)
     return st

@@ -180,6 +180,45 @@ def test_paged_prefill_validation_before_launch():
     assert call(st_ids=FAKE, starts=[8]) == la.LA_ERR_MISALIGNED_STATE
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_library_hybrid_boundary_matches_oracle(seed):
+    from oracle.boundary import hybrid_boundary
+    rng = np.random.default_rng(100 + seed)
+    for _ in range(400):
+        bt = int(rng.choice([1, 4, 16, 64]))
+        C = bt * int(rng.integers(1, 8))
+        N = int(rng.integers(1, 10 * C))
+        kv, stc = int(rng.integers(0, 10 * C)), int(rng.integers(0, 10 * C))
+        assert la.la_hybrid_boundary(N, C, bt, kv, stc) == hybrid_boundary(N, C, bt, kv, stc)
+    for bad in [(0, 16, 16, 0, 0), (10, 0, 16, 10, 10), (10, 16, 0, 10, 10), (10, 16, 16, -1, 10)]:
+        with pytest.raises(la.LinAttnError) as e:
+            la.la_hybrid_boundary(*bad)
+        assert e.value.status == la.LA_ERR_INVALID_ARG
+    with pytest.raises(la.LinAttnError) as e:
+        la.la_hybrid_boundary(5376, 1792, 48, 5376, 5376)
+    assert e.value.status == la.LA_ERR_MISALIGNED_STATE
+
+
+def test_hybrid_restore_validation_before_launch():
+    lib = la.library()
+    P = la.ctypes.c_void_p
+
+    def call(bounds, block_tokens=16, block_bytes=1024, max_blocks=8, kv_null=False, n_heads=2, bdev=True):
+        kv = la.LaKvBlocks(FAKE, 64, FAKE, 64, block_bytes, block_tokens, FAKE, FAKE, max_blocks)
+        b = np.asarray(bounds, np.int64)
+        return lib.la_hybrid_restore(None if kv_null else la.ctypes.byref(kv), len(b), n_heads, 16,
+                                     FAKE if bdev else None, P(b.ctypes.data) if len(b) else None, FAKE, 4,
+                                     FAKE, FAKE, None, None)
+    assert call([16], kv_null=True) == la.LA_ERR_INVALID_ARG
+    assert call([]) == la.LA_OK                                          # nothing to restore
+    assert call([24]) == la.LA_ERR_MISALIGNED_STATE                      # not a whole number of blocks
+    assert call([16 * 9]) == la.LA_ERR_INVALID_ARG                       # more blocks than max_blocks
+    assert call([16], block_bytes=1000) == la.LA_ERR_INVALID_ARG         # not a multiple of 16
+    assert call([16], block_tokens=0) == la.LA_ERR_INVALID_ARG
+    assert call([-16]) == la.LA_ERR_INVALID_ARG
+    assert call([16], bdev=False) == la.LA_ERR_INVALID_ARG
+
+
 def test_decode_validation_before_launch():
     lib = la.library()
     sh = la.make_shape(2, 8, 128, 128, 256)
