@@ -63,14 +63,36 @@ size_t io_size(int32_t dtype) { return dtype == LA_BF16 ? 2 : 4; }
 
 // Whether a call that runs the scan and output stages together uses the
 // single-wave scan's output wave (one kernel) instead of the split output
-// kernel; both give identical bits.  LA_SCAN_OUTPUT=0 selects the split
-// kernels (for measurement).
-bool scan_with_output() {
+// kernel; both give identical bits.  The scan-with-output workgroup holds
+// two waves with a large register file each, so fewer of them fit on a CU;
+// it is used only while every workgroup of the launch is resident at once
+// (the scan is one sequential chain per workgroup: a second round would
+// double its time).  LA_SCAN_OUTPUT=0 selects the split kernels (for
+// measurement).
+template <typename T, int DK, int DV>
+bool scan_with_output(int64_t blocks) {
     static const bool on = [] {
         const char *e = getenv("LA_SCAN_OUTPUT");
         return !(e && atoi(e) == 0);
     }();
-    return on;
+    if (!on) return false;
+    static int64_t capacity[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+        (void)hipGetLastError();
+        return false;
+    }
+    if (capacity[dev] == 0) {
+        int per_cu = 0, cus = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, la::gdr_scan1o_kernel<T, DK, DV>, 128, 0) !=
+                hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+            (void)hipGetLastError();
+            return false;
+        }
+        capacity[dev] = (int64_t)per_cu * cus;
+    }
+    return blocks <= capacity[dev];
 }
 
 // Chunks per segment of the two-level scan (1 = single-level).  A segment
@@ -263,7 +285,8 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
         if constexpr (sizeof(T) == 2) {
             if (p.seg_m > 1) return launch_two_level<T, DK, DV>(c, p, sa, max_chunks, trace);
         }
-        if (scan_variant(sizeof(T) == 4, DK) == 1 && (c.stages & LA_STAGE_OUTPUT) && scan_with_output()) {
+        if (scan_variant(sizeof(T) == 4, DK) == 1 && (c.stages & LA_STAGE_OUTPUT) &&
+            scan_with_output<T, DK, DV>(blocks)) {
             // the scan's output wave produces the output: no output launch
             hipLaunchKernelGGL((la::gdr_scan1o_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(128), 0,
                                c.stream, sa);
