@@ -67,17 +67,20 @@ __device__ inline void load_out_frag(OutFrag<T, DK> &f, const Workspace &ws, int
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
         for (int v = 0; v < VS; ++v)
-            *(uint4 *)&f.q[mt][v * VEC] = buf_load16(rq, 16u * (uint32_t)lane, 1024u * (mt * VS + v));
+            *(uint4 *)&f.q[mt][v * VEC] = buf_load16(rq, 16u * (uint32_t)lane + 1024u * (mt * VS + v), 0u);
     constexpr size_t PE = (size_t)kChunk * kChunk;   // P elements per slot-head
     const auto rp = make_rsrc((const T *)ws.p + sh * PE, PE * sizeof(T));
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
         for (int v = 0; v < VU; ++v)
-            *(uint4 *)&f.p[mt][v * VEC] = buf_load16(rp, 16u * (uint32_t)lane, 1024u * (mt * VU + v));
-    const auto rg = make_rsrc(ws.g + sh * kChunk, kChunk * sizeof(float));
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt) f.eg[mt] = buf_load4f(rg, 4u * (uint32_t)(16 * mt + c16), 0u);
+            *(uint4 *)&f.p[mt][v * VEC] = buf_load16(rp, 16u * (uint32_t)lane + 1024u * (mt * VU + v), 0u);
+    // the gates of rows c, 16 + c, 32 + c, 48 + c sit together (G layout)
+    const uint4 e = buf_load16(make_rsrc(ws.g + sh * kChunk, kChunk * sizeof(float)), 16u * (uint32_t)c16, 0u);
+    f.eg[0] = __uint_as_float(e.x);
+    f.eg[1] = __uint_as_float(e.y);
+    f.eg[2] = __uint_as_float(e.z);
+    f.eg[3] = __uint_as_float(e.w);
 }
 
 // O^T for one 16-column tile of the state: sb and ub are the scan's operand

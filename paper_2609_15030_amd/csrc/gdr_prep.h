@@ -207,7 +207,7 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
             sm.bs[lane] = b;
             sm.dW[lane] = b * __builtin_amdgcn_exp2f(gp * kLog2e);
             sm.dK[lane] = __builtin_amdgcn_exp2f((g63 - x) * kLog2e);
-            a.ws.g[sh * kChunk + lane] = x;
+            a.ws.g[sh * kChunk + 4 * (lane & 15) + (lane >> 4)] = x;   // G layout: row 16 m + c at 4 c + m
         }
     }
     __syncthreads();

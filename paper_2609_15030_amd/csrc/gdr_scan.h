@@ -485,19 +485,19 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
         const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
-            const uint4 x = buf_load16(ru, lane16, 1024u * (tile * 4 + mt));
+            const uint4 x = buf_load16(ru, lane16 + 1024u * (tile * 4 + mt), 0u);
             o.ut[mt] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
         }
         const auto rw = make_rsrc((const T *)a.ws.w + sh * L::w_elems, L::w_elems * sizeof(T));
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-            for (int v = 0; v < VS; ++v) o.wn[mt][v] = buf_load16(rw, lane16, 1024u * (mt * VS + v));
+            for (int v = 0; v < VS; ++v) o.wn[mt][v] = buf_load16(rw, lane16 + 1024u * (mt * VS + v), 0u);
         const auto rk = make_rsrc((const T *)a.ws.kt + sh * L::kt_elems, L::kt_elems * sizeof(T));
 #pragma unroll
         for (int t = 0; t < RT; ++t)
 #pragma unroll
-            for (int v = 0; v < VU; ++v) o.kt[t][v] = buf_load16(rk, lane16, 1024u * (t * VU + v));
+            for (int v = 0; v < VU; ++v) o.kt[t][v] = buf_load16(rk, lane16 + 1024u * (t * VU + v), 0u);
     };
     auto step = [&](const Ops &o, int jj) {
         const int64_t sh = (base + jj) * H + h;

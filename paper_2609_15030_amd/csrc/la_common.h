@@ -198,7 +198,8 @@ __host__ inline int64_t chunk_grid_blocks(int n_seqs, int n_heads, int64_t max_c
 //   W   : -W in A-operand order for the state contraction      [4][DK/4] x 64 lanes, io type
 //   KT  : decayed keys^T in A-operand order (chunk rows perm.) [DK/16][16] x 64 lanes, io type
 //   UT  : U~ = T diag(beta) V, C-layout per 16x16 tile        [DV/16][4] x 64 lanes x 4, fp32
-//   G   : chunk-local cumulative gate                          [64], fp32
+//   G   : chunk-local cumulative gate, row 16 m + c at 4 c + m [64], fp32
+//         (a lane's four output rows in one 16-byte load; row 63 stays at 63)
 //   SC  : state entering the chunk, B-operand order            [DV/16][DK/4] x 64 lanes, io type
 //   U   : U = U~ - W S, B-operand order                        [DV/16][16] x 64 lanes, io type
 //   P   : decayed causal Q K^T, per token tile the B operand of P^T (chunk
