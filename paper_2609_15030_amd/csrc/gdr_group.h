@@ -70,11 +70,11 @@ __global__ __launch_bounds__(64 * kGroupWaves) void gdr_group_kernel(ScanArgs a)
         const int cu0 = a.cu[seq];
         len = a.cu[seq + 1] - cu0;
         nch = n_chunks32(len, a.C, a.cps);
-        base = slot_base(cu0, seq, a.C, a.cps);
+        base = slot_base_dev(cu0, seq, a.C, a.cps);
         c0 = seg * a.seg_m;
         if (c0 >= nch) return;
         c1 = min(c0 + a.seg_m, nch);
-        seg_slot = slot_base(cu0, seq, (int64_t)a.C * a.seg_m, a.cps) + seg;
+        seg_slot = slot_base_dev(cu0, seq, (int64_t)a.C * a.seg_m, a.cps) + seg;
     }
     const int n = c1 - c0;
 

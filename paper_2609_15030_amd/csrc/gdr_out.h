@@ -141,7 +141,7 @@ __global__ __launch_bounds__(4 * DV) void gdr_out_kernel(OutArgs a) {
     chunk_range32((int)j, len, a.C, a.cps, &lo, &hi);
     const int n = hi - lo;
     const int64_t t0 = cu0 + lo;
-    const int64_t sh = (slot_base(cu0, seq, a.C, a.cps) + j) * H + h;
+    const int64_t sh = (slot_base_dev(cu0, seq, a.C, a.cps) + j) * H + h;
 
     T sb[FS], ub[FU];
     const auto rs = make_rsrc((const T *)a.ws.sc + sh * L::sc_elems, L::sc_elems * sizeof(T));

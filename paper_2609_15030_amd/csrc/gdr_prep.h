@@ -129,7 +129,7 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
     chunk_range32((int)j, len, a.C, a.cps, &lo, &hi);
     const int n = hi - lo;
     const int64_t t0 = cu0 + lo;
-    const int64_t sh = (slot_base(cu0, seq, a.C, a.cps) + j) * H + h;   // slot-head index
+    const int64_t sh = (slot_base_dev(cu0, seq, a.C, a.cps) + j) * H + h;   // slot-head index
 
     const T *kin = (const T *)a.k;
     const T *vin = (const T *)a.v;

@@ -281,7 +281,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
     const int seq = pair / H, h = pair % H;
     const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
     const int nch = n_chunks32(len, a.C, a.cps);
-    const int64_t base = slot_base(cu0, seq, a.C, a.cps);
+    const int64_t base = slot_base_dev(cu0, seq, a.C, a.cps);
     const size_t state_off = (size_t)pair * DK * DV;
     const int col = 16 * tile + c16;
 
@@ -621,7 +621,7 @@ __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
     const int seq = pair / H, h = pair % H;
     const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
     const int nch = n_chunks32(len, a.C, a.cps);
-    const int64_t base = slot_base(cu0, seq, a.C, a.cps);
+    const int64_t base = slot_base_dev(cu0, seq, a.C, a.cps);
     const size_t state_off = (size_t)pair * DK * DV;
     f32x4 S[DK / 16];
     load_state_tile<DK, DV>(start_state(a, seq, h, (size_t)DK * DV, tile == 0), tile, S);
@@ -649,7 +649,7 @@ __global__ __launch_bounds__(128) void gdr_scan1o_kernel(ScanArgs a) {
     const int seq = pair / H, h = pair % H;
     const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
     const int nch = n_chunks32(len, a.C, a.cps);
-    const int64_t base = slot_base(cu0, seq, a.C, a.cps);
+    const int64_t base = slot_base_dev(cu0, seq, a.C, a.cps);
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     if (wave == 0) {
         const size_t state_off = (size_t)pair * DK * DV;
@@ -695,7 +695,7 @@ __global__ __launch_bounds__(64) void gdr_seg_combine_kernel(ScanArgs a) {
     const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
     const int nch = n_chunks32(len, a.C, a.cps);
     const int nseg = (nch + a.seg_m - 1) / a.seg_m;
-    const int64_t sbase = slot_base(cu0, seq, (int64_t)a.C * a.seg_m, a.cps);
+    const int64_t sbase = slot_base_dev(cu0, seq, (int64_t)a.C * a.seg_m, a.cps);
     const size_t state_off = (size_t)pair * DK * DV;
     __shared__ float tr_lds[DK * kTrLd];
     f32x4 S[RT];

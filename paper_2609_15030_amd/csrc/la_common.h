@@ -162,6 +162,14 @@ __device__ __host__ inline int64_t slot_base(int64_t cu_i, int64_t i, int64_t C,
     return (cu_i * cps + (C - 1) * i) / C;
 }
 
+// Device form of slot_base: while the numerator fits 32 bits (every call
+// below 2^32 tokens-times-chunks) a 32-bit division replaces the 64-bit one.
+__device__ inline int64_t slot_base_dev(int64_t cu_i, int64_t i, int64_t C, int cps) {
+    const uint64_t num = (uint64_t)cu_i * (uint64_t)cps + (uint64_t)(C - 1) * (uint64_t)i;
+    if (num < (1ull << 32) && C < (1ll << 32)) return (int64_t)((uint32_t)num / (uint32_t)C);
+    return (int64_t)(num / (uint64_t)C);
+}
+
 __device__ __host__ inline int64_t total_slots(int64_t total_tokens, int64_t n_seqs, int64_t C,
                                                int cps) {
     return slot_base(total_tokens, n_seqs, C, cps);
@@ -177,13 +185,17 @@ __device__ __host__ inline int64_t total_slots(int64_t total_tokens, int64_t n_s
 // ---------------------------------------------------------------------------
 __device__ inline bool unit_of_block(int n_seqs, int n_heads, int max_chunks, int *seq, int *head,
                                      int64_t *chunk) {
-    const int64_t b = blockIdx.x;
-    const int64_t r = b >> 3;
-    const int64_t pair = (b & 7) + 8 * (r / max_chunks);
-    if (pair >= (int64_t)n_seqs * n_heads) return false;
-    *chunk = r % max_chunks;
-    *seq = (int)(pair / n_heads);
-    *head = (int)(pair % n_heads);
+    // 32-bit arithmetic: a 64-bit division costs hundreds of cycles at the
+    // start of every workgroup (grids and n_seqs * n_heads stay below 2^32)
+    const uint32_t b = blockIdx.x;
+    const uint32_t r = b >> 3;
+    const uint32_t q = r / (uint32_t)max_chunks;
+    const uint32_t pair = (b & 7) + 8 * q;
+    if (pair >= (uint32_t)n_seqs * (uint32_t)n_heads) return false;
+    *chunk = (int64_t)(r - q * (uint32_t)max_chunks);
+    const uint32_t sq = pair / (uint32_t)n_heads;
+    *seq = (int)sq;
+    *head = (int)(pair - sq * (uint32_t)n_heads);
     return true;
 }
 
