@@ -209,6 +209,35 @@ def bench_host_tier(la, torch, stream_ptr, events, sizes=(112, 4096), page_elems
     return out
 
 
+def bench_workloads(api, torch, stream_ptr, events, reps=10):
+    """Cold prefill (checkpoints to a dense array) of the larger workloads,
+    where many chains run side by side: the 16-head 32K-token prefill and
+    the 16-sequence varlen batch.  Tokens/s counts every token of the call;
+    TFLOP/s uses the algorithmic flops per token-head."""
+    from paper_2609_15030_amd import workloads as wl
+    out = {}
+    for w in (wl.long_prefill(), wl.batched_varlen()):
+        x = w.inputs
+        xd = api.to_device(x)
+        pf = api.Prefill(xd, w.interval)
+        for _ in range(2):
+            pf.run()
+        torch.cuda.synchronize()
+        events.record(4, stream_ptr)
+        for _ in range(reps):
+            pf.run()
+        events.record(5, stream_ptr)
+        us = events.ms(4, 5) / reps * 1e3
+        T = x.total_tokens
+        fl = sum(flops_per_token_head(x.dk, x.dv).values()) * T * x.n_heads
+        out[w.name] = {"tokens": T, "heads": x.n_heads, "ckpt_interval": w.interval, "us": round(us, 1),
+                       "tokens_per_s": round(T / (us * 1e-6), 1),
+                       "alg_tflops": round(fl / (us * 1e-6) / 1e12, 2),
+                       "frac_bf16_peak": round(fl / (us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4)}
+        del pf, xd
+    return out
+
+
 KV_TOKEN_BYTES = 8268    # attention entries per token per rank, fixed by the paper's reload byte counts
 KV_BLOCK_TOKENS = 16
 
@@ -298,6 +327,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-pool", action="store_true")
+    ap.add_argument("--no-workloads", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this path holds one tensor-parallel rank's heads and "
@@ -412,6 +442,8 @@ def main():
     if not args.no_pool:
         out["host_tier"] = bench_host_tier(la, torch, sp, ev)
         out["hybrid_restore"] = bench_hybrid(la, torch, sp, ev, N, C, H)
+    if not args.no_workloads:
+        out["workloads"] = bench_workloads(api, torch, sp, ev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, B, args.cpu_seconds)
     print(json.dumps(out), flush=True)
