@@ -40,6 +40,43 @@ struct PrepArgs {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// Cross-lane moves (DPP): CTRL selects the source lane, ROWS enables rows of
+// 16 lanes; lanes without a source, and disabled rows, read 0.
+template <int CTRL, int ROWS = 0xF>
+__device__ inline float dpp_f(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWS, 0xF, true));
+}
+
+// Inclusive prefix sum over the wave's 64 lanes: shifts within each row of
+// 16 lanes, then each row's carry from the rows before it (row broadcasts).
+__device__ inline float wave_inclusive_sum(float x) {
+    x += dpp_f<0x111>(x);          // row_shr:1
+    x += dpp_f<0x112>(x);          // row_shr:2
+    x += dpp_f<0x114>(x);          // row_shr:4
+    x += dpp_f<0x118>(x);          // row_shr:8
+    x += dpp_f<0x142, 0xA>(x);     // row_bcast:15 into rows 1 and 3
+    x += dpp_f<0x143, 0xC>(x);     // row_bcast:31 into rows 2 and 3
+    return x;
+}
+
+// One column-oriented step of the diagonal-block substitution: lane s of
+// each row holds the final x[s] of its columns; broadcast it along the row
+// (row_newbcast:s) and subtract L[r][s] x[s] (L is zero at and above the
+// diagonal, so rows r <= s are left unchanged).
+template <int S>
+__device__ inline void subst_step(float (&x)[4], const float (&L)[16]) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) x[c] -= L[S] * dpp_f<0x150 + S>(x[c]);
+}
+
+template <int S = 0>
+__device__ inline void subst_all(float (&x)[4], const float (&L)[16]) {
+    if constexpr (S < 16) {
+        subst_step<S>(x, L);
+        subst_all<S + 1>(x, L);
+    }
+}
+
 template <typename T, int DK, int DV> struct alignas(16) PrepSmem {
     static constexpr int PK = Vec<T>::N;       // row pads keep 16-byte alignment
     static constexpr int DM = DK > DV ? DK : DV;
@@ -192,16 +229,11 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
         }
         // ---- 2. chunk-local gate prefix sum (wave 0) --------------------------
         if (wave == 0) {
-            float x = tid < n ? gv : 0.f;
             const float b = tid < n ? bv : 0.f;
-#pragma unroll
-            for (int d = 1; d < 64; d <<= 1) {
-                const float y = __shfl_up(x, d, 64);
-                if (lane >= d) x += y;
-            }
-            const float prev = __shfl_up(x, 1, 64);
-            const float gp = (a.variant == 0) ? (lane == 0 ? 0.f : prev) : x;
-            const float g63 = __shfl(x, 63, 64);
+            const float x = wave_inclusive_sum(tid < n ? gv : 0.f);
+            const float prev = dpp_f<0x138>(x);   // wave_shr:1: lane - 1's sum, 0 on lane 0
+            const float gp = (a.variant == 0) ? prev : x;
+            const float g63 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
             sm.G2[lane] = x * kLog2e;
             sm.Gp2[lane] = gp * kLog2e;
             sm.bs[lane] = b;
@@ -249,34 +281,26 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
     __syncthreads();
 
     // ---- 4. X = (I + A)^{-1}: diagonal 16-blocks by substitution ---------------
+    // Wave w inverts block w with all 64 lanes: lane (q, r), q = lane / 16,
+    // r = lane % 16, holds row r of columns 4q .. 4q + 3 of the block's
+    // inverse.  Each x[r] receives the updates L[r][s] x[s] in the order
+    // s = 0, 1, ..., as forward substitution does.
     {
-        const int base = 16 * wave;
-        // the block's strictly lower part, read once (same addresses on all lanes)
-        float ab[16][16];
+        const int base = 16 * wave, q = lane >> 4, r = lane & 15;
+        float L[16];
 #pragma unroll
-        for (int r = 1; r < 16; ++r)
-#pragma unroll
-            for (int s4 = 0; s4 < 16; s4 += 4) {
-                if (s4 < r) {
-                    const float4 v = *(const float4 *)&sm.am[base + r][base + s4];
-                    ab[r][s4] = v.x;
-                    ab[r][s4 + 1] = v.y;
-                    ab[r][s4 + 2] = v.z;
-                    ab[r][s4 + 3] = v.w;
-                }
-            }
-        if (lane < 16) {
-            float x[16];
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float acc = (r == lane) ? 1.f : 0.f;
-#pragma unroll
-                for (int s = 0; s < r; ++s) acc -= ab[r][s] * x[s];
-                x[r] = acc;
-            }
-#pragma unroll
-            for (int r = 0; r < 16; ++r) sm.xm[base + r][base + lane] = x[r];
+        for (int s4 = 0; s4 < 16; s4 += 4) {
+            const float4 v = *(const float4 *)&sm.am[base + r][base + s4];
+            L[s4] = v.x;
+            L[s4 + 1] = v.y;
+            L[s4 + 2] = v.z;
+            L[s4 + 3] = v.w;
         }
+        float x[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) x[c] = (r == 4 * q + c) ? 1.f : 0.f;
+        subst_all(x, L);
+        *(float4 *)&sm.xm[base + r][base + 4 * q] = make_float4(x[0], x[1], x[2], x[3]);
     }
     __syncthreads();
     // off-diagonal blocks by bands: X_ij = -X_ii sum_{k=j}^{i-1} A_ik X_kj
@@ -290,7 +314,11 @@ __global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) sm.ysc[wave][4 * g16 + i][c16] = y[i];
         }
-        __syncthreads();
+        // ysc[wave] is written and read by this wave alone: its LDS accesses
+        // execute in order, so only the compiler needs holding back here
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         if (active) {
             f32x4 xij = mm16_f32(&sm.xm[16 * bi][16 * bi], LDA, &sm.ysc[wave][0][0], 17, zero4(), lane);
 #pragma unroll
