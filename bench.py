@@ -8,11 +8,19 @@ checkpoint interval C = 256):
   1. strict-prefix boundary on the host: B = 3,328 for N = 3,584;
   2. cold prefill of all 3,584 tokens, its 14 x 8 fp32 checkpoint pages
      written straight into a pool through a random-permutation page table
-     (the paged save folded into the scan, la_prefill_paged);
+     (the paged save folded into the scan);
   3. resume over the 256-token suffix [B, N), its starting state read
      straight from the 8 pages of the checkpoint at B (the paged restore
-     folded into the scan) and its checkpoint at N written to that
-     prefix's pages.
+     folded into the scan) and its checkpoint at N written to a page.
+
+Steps 2 and 3 are two requests that a serving step batches: they go to the
+library as one la_prefill_paged call over two sequences (start 0 and start
+B).  The resume starts from the checkpoint page of prefix B that the
+previous step's cold run wrote: the pool holds two page regions written on
+alternate steps, so no page is read and written in the same call (the
+call's contract).  The same step issued as two calls, the resume reading
+the page its step's cold run has just written, is timed as well
+("serial_calls").
 
 Beside the step it reports, each on its own timer: paged save/restore
 bandwidth on the full 4,096-page pool, decode continuation (one token per
@@ -124,7 +132,7 @@ def measured_traffic(kernel):
     if rec.get("source_sha256") != h.hexdigest():
         return None
     for r in rec["records"]:
-        if r["kernel"] == kernel and r["role"] == "cold":
+        if r["kernel"] == kernel and r["role"] == "step":
             return r["read_bytes"] + r["write_bytes"]
     return None
 
@@ -207,6 +215,35 @@ def bench_host_tier(la, torch, stream_ptr, events, sizes=(112, 4096), page_elems
                              "h2d_GBps": round(nbytes / (ms_r / reps * 1e-3) / 1e9, 1),
                              "d2h_us": round(ms_s / reps * 1e3, 1), "h2d_us": round(ms_r / reps * 1e3, 1)}
     return out
+
+
+def bench_serial_step(api, la, torch, x, B, C, N, H, dk, dv, steps):
+    """The step as two calls: the cold prefill (checkpoints into the pool),
+    then the resume, its starting state read from the page of prefix B the
+    cold run has just written.  Whole-step tokens/s over back-to-back steps."""
+    cold = api.Prefill(api.to_device(x), C, emit_ckpt=False)
+    resume = api.Prefill(api.to_device(x.tokens(B, N)), C, starts=[B], emit_ckpt=False)
+    n_ck = cold.n_ckpt_rows
+    pool = torch.empty((n_ck * H, dk * dv), dtype=torch.float32, device="cuda")
+    save_ids = torch.from_numpy(np.random.default_rng(12).permutation(n_ck * H).astype(np.int32)).cuda()
+    j = B // C - 1
+    restore_ids = save_ids[j * H:(j + 1) * H].contiguous()
+    resume_ck_ids = save_ids[(j + 1) * H:(j + 1 + resume.n_ckpt_rows) * H].contiguous()
+
+    def step():
+        cold.run_paged(pool, ckpt_page_ids=save_ids)
+        resume.run_paged(pool, ckpt_page_ids=resume_ck_ids, state_page_ids=restore_ids)
+
+    for _ in range(5):
+        step()
+    torch.cuda.synchronize()
+    assert torch.equal(resume.o, cold.o[B:]) and torch.equal(resume.final, cold.final)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    return {"ms_per_step": round(dt * 1e3, 4), "tokens_per_s": round((N + N - B) / dt, 1)}
 
 
 def bench_workloads(api, torch, stream_ptr, events, reps=10):
@@ -344,41 +381,45 @@ def main():
     x, C = w.inputs, w.interval
     N, H, dk, dv = x.total_tokens, x.n_heads, x.dk, x.dv
     B = la.strict_prefix_boundary(N, C, w.available[0])
-    xd = api.to_device(x)
-    xs = api.to_device(x.tokens(B, N))
-    cold = api.Prefill(xd, C, emit_ckpt=False)
-    resume = api.Prefill(xs, C, starts=[B], emit_ckpt=False)
-    n_ck = cold.n_ckpt_rows
+    from paper_2609_15030_amd.workloads import Inputs
+    xr = x.tokens(B, N)
+    cat = lambda a, b: np.ascontiguousarray(np.concatenate([a, b]))
+    batch = Inputs(cat(x.q, xr.q), cat(x.k, xr.k), cat(x.v, xr.v), cat(x.g, xr.g), cat(x.beta, xr.beta),
+                   np.array([0, N, N + (N - B)], np.int32), x.io_dtype)
+    both = api.Prefill(api.to_device(batch), C, starts=[0, B], emit_ckpt=False)
+    rows = both.n_ckpt_rows                  # 14 of the cold run, 1 of the resume
     rng = np.random.default_rng(11)
-    pool = torch.empty((n_ck * H, dk * dv), dtype=torch.float32, device="cuda")
-    save_ids = torch.from_numpy(rng.permutation(n_ck * H).astype(np.int32)).cuda()
-    j = B // C - 1
-    # the resume starts from the page of prefix B and writes the checkpoint
-    # pages of its own prefixes (B + C, ...): the cold run's pages for those
-    restore_ids = save_ids[j * H:(j + 1) * H].contiguous()
-    resume_ck_ids = save_ids[(j + 1) * H:(j + 1 + resume.n_ckpt_rows) * H].contiguous()
+    pool = torch.zeros((2 * rows * H, dk * dv), dtype=torch.float32, device="cuda")
+    perm = rng.permutation(2 * rows * H).astype(np.int32)
+    region = [torch.from_numpy(perm[r * rows * H:(r + 1) * rows * H]).cuda() for r in (0, 1)]
+    j = B // C - 1                            # the cold run's checkpoint row of prefix B
+    cold_start = torch.full((H,), -1, dtype=torch.int32, device="cuda")
+    # the resume (sequence 1) starts from the page the other region's cold run wrote
+    state_ids = [torch.cat([cold_start, region[1 - r][j * H:(j + 1) * H]]).contiguous() for r in (0, 1)]
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     ev = HipEvents(10)
     stage_ev = [ev.ev[0], ev.ev[1], ev.ev[2], ev.ev[3]]
+    k_step = [0]
 
     def step(trace):
         b = la.strict_prefix_boundary(N, C, w.available[0])
         assert b == B
+        r = k_step[0] % 2
+        k_step[0] += 1
         if trace:
             la.la_trace_set_events(stage_ev)
-        # cold prefill: checkpoints straight into the pool's pages (the save)
-        cold.run_paged(pool, ckpt_page_ids=save_ids)
+        # checkpoints straight into region r's pages (the save); the resume's
+        # starting state straight from the other region's page of prefix B (the restore)
+        both.run_paged(pool, ckpt_page_ids=region[r], state_page_ids=state_ids[r])
         if trace:
             la.la_trace_set_events([])
-        # reload: the resume reads its starting state straight from the page (the restore)
-        resume.run_paged(pool, ckpt_page_ids=resume_ck_ids, state_page_ids=restore_ids)
 
-    for _ in range(args.warmup):
+    for _ in range(max(args.warmup, 2)):      # two steps fill both regions
         step(False)
     torch.cuda.synchronize()
-    # parity guard on the benchmarked buffers: resume equals the cold run's tail
-    assert torch.equal(resume.o, cold.o[B:]) and torch.equal(resume.final, cold.final)
+    # parity guard on the benchmarked buffers: the resume equals the cold run's tail
+    assert torch.equal(both.o[N:], both.o[B:N]) and torch.equal(both.final[1], both.final[0])
 
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -391,8 +432,9 @@ def main():
     gpu_ms = ev.ms(8, 9)
     ms_per_step = wall * 1e3 / args.steps
     tokens_per_step = N + (N - B)
+    serial = bench_serial_step(api, la, torch, x, B, C, N, H, dk, dv, args.steps)
 
-    # per-kernel durations of the cold prefill, from events inside the library
+    # per-kernel durations of the step's call, from events inside the library
     stage = {"prep": 0.0, "scan": 0.0, "out": 0.0}
     n_trace = max(10, args.steps // 2)
     for _ in range(n_trace):
@@ -409,14 +451,14 @@ def main():
     # events with no kernel between them)
     kfl = dict(fl, scan=fl["scan"] + fl["out"], out=0.0) if fused else fl
     dom = max(("prep", "scan", "out"), key=stage_us.get)
-    achieved = kfl[dom] * N * H / (stage_us[dom] * 1e-6) / 1e12
+    achieved = kfl[dom] * tokens_per_step * H / (stage_us[dom] * 1e-6) / 1e12
     prefill_us = sum(stage_us.values())
     kname = {"prep": "gdr_prep_kernel", "scan": scan_name, "out": "gdr_out_kernel"}[dom]
     roofline = {"bound": "mfma", "kernel": kname,
                 "achieved": round(achieved, 3), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_PEAK_TFLOPS, 5), "traffic": measured_traffic(kname),
                 "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)",
-                "flops_per_launch": kfl[dom] * N * H, "avg_launch_us": round(stage_us[dom], 2)}
+                "flops_per_launch": kfl[dom] * tokens_per_step * H, "avg_launch_us": round(stage_us[dom], 2)}
 
     out = {
         "metric": "linear-attn prefill tokens/s per rank + % MFMA peak; state save/restore GB/s",
@@ -430,10 +472,11 @@ def main():
                    "chunk": CHUNK, "ckpt_interval": C, "restore_at": B,
                    "tokens_per_step": tokens_per_step},
         "gpu_ms_per_step": round(gpu_ms / args.steps, 4),
-        "cold_prefill": {"us": round(prefill_us, 2), "tokens_per_s": round(N / (prefill_us * 1e-6), 1),
-                         "stage_us": {k: round(v, 2) for k, v in stage_us.items()},
-                         "scan_kernel": scan_name, "output_in_scan": fused,
-                         "alg_tflops": round(sum(fl.values()) * N * H / (prefill_us * 1e-6) / 1e12, 3)},
+        "step_call": {"us": round(prefill_us, 2), "tokens_per_s": round(tokens_per_step / (prefill_us * 1e-6), 1),
+                      "stage_us": {k: round(v, 2) for k, v in stage_us.items()},
+                      "scan_kernel": scan_name, "output_in_scan": fused,
+                      "alg_tflops": round(sum(fl.values()) * tokens_per_step * H / (prefill_us * 1e-6) / 1e12, 3)},
+        "serial_calls": serial,
         "roofline": roofline,
     }
     if not args.no_pool:
