@@ -144,8 +144,10 @@ template <> struct RowTile<float> {
     }
 };
 
+// Two workgroups per CU where the LDS allows (fp32 operands with a
+// 128-wide head dimension need more than half of it).
 template <typename T, int DK, int DV>
-__global__ __launch_bounds__(256, 2) void gdr_prep_kernel(PrepArgs a) {
+__global__ __launch_bounds__(256, sizeof(PrepSmem<T, DK, DV>) <= 80 * 1024 ? 2 : 1) void gdr_prep_kernel(PrepArgs a) {
     using M = MT<T>;
     using RT = RowTile<T>;
     using Sm = PrepSmem<T, DK, DV>;

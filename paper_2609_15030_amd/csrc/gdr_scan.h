@@ -51,6 +51,18 @@ struct PageIO {
     int32_t n_pages;
 };
 
+// Dispatch order of the (sequence, head) chains: the chain of rank k is
+// pair[k] when n > 0, else pair k.  The host ranks chains by length,
+// longest first: workgroups are dealt to XCDs round-robin and, within an
+// XCD, to its CUs in dispatch order, so the long chains start first and
+// each CU's share of chain-chunks evens out (a scan workgroup's chunk step
+// is bound by its CU's memory pipe, which the workgroups on that CU share).
+constexpr int kChainOrderMax = 1024;
+struct ChainOrder {
+    int32_t n;
+    uint16_t pair[kChainOrderMax];
+};
+
 struct ScanArgs {
     const int32_t *cu;
     const float *state_in;        // [n_seqs, H, DK, DV] or null (zero state)
@@ -64,7 +76,14 @@ struct ScanArgs {
     void *o;                      // scan with output wave only: output [T, H, dv] (io type)
     float scale;
     PageIO pg;
+    ChainOrder order;
 };
+
+// The chain of workgroup rank k (see ChainOrder); -1 past the last chain.
+__device__ inline int chain_of_rank(const ScanArgs &a, int k) {
+    if (k >= a.n_seqs * a.n_heads) return -1;
+    return a.order.n > 0 ? (int)a.order.pair[k] : k;
+}
 
 // Counts an id outside [-1, n_pages) once: count is set in one wave per
 // (sequence, head), and one lane adds.
@@ -275,9 +294,9 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
     // NT workgroups of one (sequence, head) land on one XCD and share the
     // chunk operands through its L2.
     const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
-    const int pair = xcd + 8 * (q / NT), tile = q % NT;
+    const int pair = chain_of_rank(a, xcd + 8 * (q / NT)), tile = q % NT;
     const int H = a.n_heads;
-    if (pair >= a.n_seqs * H) return;
+    if (pair < 0) return;
     const int seq = pair / H, h = pair % H;
     const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
     const int nch = n_chunks32(len, a.C, a.cps);
@@ -615,9 +634,9 @@ template <typename T, int DK, int DV>
 __global__ __launch_bounds__(64) void gdr_scan1_kernel(ScanArgs a) {
     constexpr int NT = DV / 16;
     const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
-    const int pair = xcd + 8 * (q / NT), tile = q % NT;
+    const int pair = chain_of_rank(a, xcd + 8 * (q / NT)), tile = q % NT;
     const int H = a.n_heads;
-    if (pair >= a.n_seqs * H) return;
+    if (pair < 0) return;
     const int seq = pair / H, h = pair % H;
     const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
     const int nch = n_chunks32(len, a.C, a.cps);
@@ -643,9 +662,9 @@ __global__ __launch_bounds__(128) void gdr_scan1o_kernel(ScanArgs a) {
     constexpr int NT = DV / 16;
     __shared__ Handoff<T, DK> hs;
     const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
-    const int pair = xcd + 8 * (q / NT), tile = q % NT;
+    const int pair = chain_of_rank(a, xcd + 8 * (q / NT)), tile = q % NT;
     const int H = a.n_heads;
-    if (pair >= a.n_seqs * H) return;
+    if (pair < 0) return;
     const int seq = pair / H, h = pair % H;
     const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
     const int nch = n_chunks32(len, a.C, a.cps);
@@ -688,9 +707,9 @@ __global__ __launch_bounds__(64) void gdr_seg_combine_kernel(ScanArgs a) {
     constexpr int kMfmas = RT * (FS / KW), kLoads = 1 + RT + RT * VS;
     const int lane = threadIdx.x, g16 = lane >> 4, c16 = lane & 15;
     const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
-    const int pair = xcd + 8 * (q / NT), tile = q % NT;
+    const int pair = chain_of_rank(a, xcd + 8 * (q / NT)), tile = q % NT;
     const int H = a.n_heads;
-    if (pair >= a.n_seqs * H) return;
+    if (pair < 0) return;
     const int seq = pair / H, h = pair % H;
     const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
     const int nch = n_chunks32(len, a.C, a.cps);

@@ -241,6 +241,27 @@ la_status launch_two_level(const PrefillCall &c, const WsPlan &p, la::ScanArgs s
     return launch_out<T, DK, DV>(c, sa.ws, max_chunks, trace);
 }
 
+// Ranks the (sequence, head) chains for dispatch, longest first (equal
+// lengths keep sequence order), so the workgroups each CU receives mix long
+// and short chains.  Batches of more than kChainOrderMax chains, or of one
+// sequence, keep the natural order.
+void order_chains(const PrefillCall &c, la::ChainOrder &order) {
+    const la_shape *s = c.shape;
+    const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
+    order.n = 0;
+    if (s->n_seqs < 2 || pairs > la::kChainOrderMax) return;
+    const int cps = la::chunks_per_interval(s->ckpt_interval);
+    int64_t nch[la::kChainOrderMax];
+    for (int i = 0; i < s->n_seqs; ++i)
+        nch[i] = la::n_chunks((int64_t)c.cu_host[i + 1] - c.cu_host[i], s->ckpt_interval, cps);
+    int32_t idx[la::kChainOrderMax];
+    for (int64_t k = 0; k < pairs; ++k) idx[k] = (int32_t)k;
+    const int H = s->n_heads;
+    std::stable_sort(idx, idx + pairs, [&](int32_t x, int32_t y) { return nch[x / H] > nch[y / H]; });
+    for (int64_t k = 0; k < pairs; ++k) order.pair[k] = (uint16_t)idx[k];
+    order.n = (int32_t)pairs;
+}
+
 template <typename T, int DK, int DV>
 la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) {
     const la_shape *s = c.shape;
@@ -282,6 +303,7 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
         constexpr int NT = DV / 16;
         const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
         const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
+        order_chains(c, sa.order);
         if constexpr (sizeof(T) == 2) {
             if (p.seg_m > 1) return launch_two_level<T, DK, DV>(c, p, sa, max_chunks, trace);
         }
