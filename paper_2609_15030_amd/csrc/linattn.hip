@@ -95,6 +95,22 @@ bool scan_with_output(int64_t blocks) {
     return blocks <= capacity[dev];
 }
 
+// Whether a single-level bf16 scan runs as one workgroup per (sequence,
+// head) chain (the chunk operands shared through LDS, output waves beside
+// the scan waves) instead of one wave per 16-column tile.  By default the
+// workgroup form serves the calls that include the output stage and whose
+// per-tile scan with output wave would not be resident at once; without it
+// the output would make a round trip through HBM.  LA_SCAN_GROUP=1|0 forces
+// the choice (for measurement).
+bool scan_by_group(bool tile_scan_with_output, bool output_stage) {
+    static const int forced = [] {
+        const char *e = getenv("LA_SCAN_GROUP");
+        return e ? atoi(e) : -1;
+    }();
+    if (forced == 0 || forced == 1) return forced == 1;
+    return output_stage && !tile_scan_with_output;
+}
+
 // Chunks per segment of the two-level scan (1 = single-level).  A segment
 // must divide a checkpoint interval's chunks, so every checkpoint position is
 // a segment boundary and a resume from a checkpoint sees the same segments
@@ -233,12 +249,20 @@ la_status launch_two_level(const PrefillCall &c, const WsPlan &p, la::ScanArgs s
     hipLaunchKernelGGL((la::gdr_seg_combine_kernel<T, DK, DV>), dim3((unsigned)(8 * NT * ((pairs + 7) / 8))),
                        dim3(64), 0, c.stream, sa);
     if (la_status e = hip_check("segment combine launch")) return e;
+    // the replay's output waves produce the output when the call includes
+    // the output stage; otherwise the split output kernel reads the states
+    // and U the replay leaves in the workspace
+    const bool out_stage = (c.stages & LA_STAGE_OUTPUT) != 0;
     if (units > 0) {
-        hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupReplay>), dim3((unsigned)units),
-                           dim3(64 * la::kGroupWaves), 0, c.stream, sa);
+        if (out_stage)
+            hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupReplay, true>), dim3((unsigned)units),
+                               dim3(128 * la::kGroupWaves), 0, c.stream, sa);
+        else
+            hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupReplay>), dim3((unsigned)units),
+                               dim3(64 * la::kGroupWaves), 0, c.stream, sa);
         if (la_status e = hip_check("segment replay launch")) return e;
     }
-    return launch_out<T, DK, DV>(c, sa.ws, max_chunks, trace);
+    return launch_out<T, DK, DV>(c, sa.ws, out_stage ? 0 : max_chunks, trace);
 }
 
 // Ranks the (sequence, head) chains for dispatch, longest first (equal
@@ -307,8 +331,25 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
         if constexpr (sizeof(T) == 2) {
             if (p.seg_m > 1) return launch_two_level<T, DK, DV>(c, p, sa, max_chunks, trace);
         }
-        if (scan_variant(sizeof(T) == 4, DK) == 1 && (c.stages & LA_STAGE_OUTPUT) &&
-            scan_with_output<T, DK, DV>(blocks)) {
+        const bool out_stage = (c.stages & LA_STAGE_OUTPUT) != 0;
+        const bool with_out = scan_variant(sizeof(T) == 4, DK) == 1 && out_stage && scan_with_output<T, DK, DV>(blocks);
+        if constexpr (sizeof(T) == 2) {
+            if (scan_by_group(with_out, out_stage)) {
+                // one workgroup per (sequence, head) chain: 4 scan waves, and
+                // 4 output waves when the call includes the output stage
+                sa.seg_m = 1;
+                sa.max_seg = 1;
+                if (out_stage)
+                    hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupScan, true>), dim3((unsigned)pairs),
+                                       dim3(128 * la::kGroupWaves), 0, c.stream, sa);
+                else
+                    hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupScan>), dim3((unsigned)pairs),
+                                       dim3(64 * la::kGroupWaves), 0, c.stream, sa);
+                if (la_status e = hip_check("inter-chunk scan launch")) return e;
+                return launch_out<T, DK, DV>(c, ws, 0, trace);
+            }
+        }
+        if (with_out) {
             // the scan's output wave produces the output: no output launch
             hipLaunchKernelGGL((la::gdr_scan1o_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(128), 0,
                                c.stream, sa);
