@@ -201,15 +201,17 @@ def bench_host_tier(la, torch, stream_ptr, events, sizes=(112, 4096), page_elems
         la.la_state_restore_host(pool, perm, back)
         torch.cuda.synchronize()
         assert torch.equal(back, states)
-        ms_s = ms_r = 0.0
-        for _ in range(reps):
-            events.record(4, stream_ptr)
+        # every repetition queued before the first event is read (see bench_pool)
+        ev = HipEvents(2 * reps + 1)
+        la.la_state_restore_host(pool, perm, back)
+        ev.record(0, stream_ptr)
+        for r in range(reps):
             la.la_state_save_host(states, pool, perm)
-            events.record(5, stream_ptr)
+            ev.record(2 * r + 1, stream_ptr)
             la.la_state_restore_host(pool, perm, back)
-            events.record(6, stream_ptr)
-            ms_s += events.ms(4, 5)
-            ms_r += events.ms(5, 6)
+            ev.record(2 * r + 2, stream_ptr)
+        ms_s = sum(ev.ms(2 * r, 2 * r + 1) for r in range(reps))
+        ms_r = sum(ev.ms(2 * r + 1, 2 * r + 2) for r in range(reps))
         nbytes = n * page_elems * 4
         out[f"{n}_pages"] = {"bytes": nbytes, "d2h_GBps": round(nbytes / (ms_s / reps * 1e-3) / 1e9, 1),
                              "h2d_GBps": round(nbytes / (ms_r / reps * 1e-3) / 1e9, 1),
@@ -260,6 +262,7 @@ def bench_workloads(api, torch, stream_ptr, events, reps=10):
         for _ in range(2):
             pf.run()
         torch.cuda.synchronize()
+        pf.run()   # busy queue at the start event
         events.record(4, stream_ptr)
         for _ in range(reps):
             pf.run()
@@ -311,6 +314,8 @@ def bench_hybrid(la, torch, stream_ptr, events, n_tokens, interval, n_heads, pag
         torch.cuda.synchronize()
         # back-to-back launches: the entry point's host-side checks of the pools
         # overlap the previous launch instead of idling the GPU between events
+        # (one more launch queued first, so the GPU is busy at the start event)
+        la.la_hybrid_restore(kv, bdev, [B], stp, sid, states, n_heads)
         events.record(4, stream_ptr)
         for _ in range(reps):
             la.la_hybrid_restore(kv, bdev, [B], stp, sid, states, n_heads)
@@ -337,15 +342,19 @@ def bench_pool(la, torch, stream_ptr, events, n_pages=4096, page_elems=128 * 128
         la.la_state_restore_paged(pool, perm, back)
     torch.cuda.synchronize()
     assert torch.equal(back, states)
-    ms_save = ms_restore = 0.0
-    for _ in range(reps):
-        events.record(4, stream_ptr)
+    # All repetitions are queued before the first event is read: waiting on
+    # each repetition would leave the GPU idle at every save's start event,
+    # and the save's interval would then hold the host's launch latency.
+    ev = HipEvents(2 * reps + 1)
+    la.la_state_restore_paged(pool, perm, back)   # the queue is busy when the first event is recorded
+    ev.record(0, stream_ptr)
+    for r in range(reps):
         la.la_state_save_paged(states, pool, perm)
-        events.record(5, stream_ptr)
+        ev.record(2 * r + 1, stream_ptr)
         la.la_state_restore_paged(pool, perm, back)
-        events.record(6, stream_ptr)
-        ms_save += events.ms(4, 5)
-        ms_restore += events.ms(5, 6)
+        ev.record(2 * r + 2, stream_ptr)
+    ms_save = sum(ev.ms(2 * r, 2 * r + 1) for r in range(reps))
+    ms_restore = sum(ev.ms(2 * r + 1, 2 * r + 2) for r in range(reps))
     nbytes = 2.0 * n_pages * page_elems * 4           # read + write
     save = nbytes / (ms_save / reps * 1e-3) / 1e9
     restore = nbytes / (ms_restore / reps * 1e-3) / 1e9
