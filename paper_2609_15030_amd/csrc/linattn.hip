@@ -63,12 +63,16 @@ size_t io_size(int32_t dtype) { return dtype == LA_BF16 ? 2 : 4; }
 
 // Whether a call that runs the scan and output stages together uses the
 // single-wave scan's output wave (one kernel) instead of the split output
-// kernel; both give identical bits.  The scan-with-output workgroup holds
-// two waves with a large register file each, so fewer of them fit on a CU;
-// it is used only while every workgroup of the launch is resident at once
-// (the scan is one sequential chain per workgroup: a second round would
-// double its time).  LA_SCAN_OUTPUT=0 selects the split kernels (for
-// measurement).
+// kernel or the workgroup scan; all give identical bits.  The
+// scan-with-output workgroup holds two waves with a large register file
+// each, so few of them fit on a CU, and each is one sequential chain: a
+// launch that needs more rounds of residency than it has chains per round
+// runs its later chains after the first ones end.  fp32 operands use it
+// only while every workgroup is resident at once; bf16 up to two rounds
+// (on a 16-sequence, 8-head batch of 1,024 tiles with 512 resident it beat
+// both the split kernels, whose state and U make a round trip through HBM,
+// and the workgroup scan, bound by its CU's LDS bandwidth).
+// LA_SCAN_OUTPUT=0 selects the split kernels (for measurement).
 template <typename T, int DK, int DV>
 bool scan_with_output(int64_t blocks) {
     static const bool on = [] {
@@ -92,16 +96,17 @@ bool scan_with_output(int64_t blocks) {
         }
         capacity[dev] = (int64_t)per_cu * cus;
     }
-    return blocks <= capacity[dev];
+    const int64_t rounds = sizeof(T) == 2 ? 2 : 1;
+    return blocks <= rounds * capacity[dev];
 }
 
 // Whether a single-level bf16 scan runs as one workgroup per (sequence,
 // head) chain (the chunk operands shared through LDS, output waves beside
 // the scan waves) instead of one wave per 16-column tile.  By default the
-// workgroup form serves the calls that include the output stage and whose
-// per-tile scan with output wave would not be resident at once; without it
-// the output would make a round trip through HBM.  LA_SCAN_GROUP=1|0 forces
-// the choice (for measurement).
+// workgroup form serves the calls that include the output stage and have
+// more tiles than the per-tile scan with output wave takes (see
+// scan_with_output); the split kernels' output would make a round trip
+// through HBM.  LA_SCAN_GROUP=1|0 forces the choice (for measurement).
 bool scan_by_group(bool tile_scan_with_output, bool output_stage) {
     static const int forced = [] {
         const char *e = getenv("LA_SCAN_GROUP");

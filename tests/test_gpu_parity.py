@@ -193,3 +193,42 @@ def test_prefix_double_application_is_detected():
     good = api.prefill_resume(api.to_device(x.tokens(B, N)), [B], res.ckpt[B // C - 1:B // C].clone(), C)
     torch.cuda.synchronize()
     assert state_err(host(good.final_state), fin_ref) <= TOL[la.LA_BF16]
+
+
+def test_many_chains_workgroup_scan():
+    """A batch of 320 (sequence, head) chains, 2,560 column tiles: more than
+    the per-tile scan with output wave takes, so the scan runs one workgroup
+    per chain with output waves beside it.  Parity with the oracle; a
+    sequence alone (per-tile scan) gives the same bits as inside the batch;
+    and every sequence resumed at its strict-prefix boundary from the
+    batch's own checkpoints reproduces the cold run's tail and final state
+    bit for bit."""
+    rng = np.random.default_rng(511)
+    lens = [int(n) for n in rng.integers(1, 400, size=40)]
+    H, C = 8, 64
+    x = wl.random_inputs(511, lens, H, 128, 128, wl.BF16)
+    xd, res = _run_cold(x, C)
+    ref = oracle_run(x, interval=C)
+    compare(res, ref, x.cu_seqlens, TOL[la.LA_BF16], "40 seqs x 8 heads, workgroup scan")
+    cu = x.cu_seqlens
+    i = int(np.argmax(lens))
+    alone = api.prefill(api.to_device(x.seq(i)), C)
+    torch.cuda.synchronize()
+    s, e = int(cu[i]), int(cu[i + 1])
+    off = int(res.ckpt_offsets[i])
+    assert torch.equal(alone.o, res.o[s:e]) and torch.equal(alone.final_state[0], res.final_state[i])
+    assert torch.equal(alone.ckpt, res.ckpt[off:off + alone.n_ckpt_rows])
+    # strict-prefix resume of every sequence from the batch's checkpoints
+    starts = [la.strict_prefix_boundary(n, C, n) for n in lens]
+    rows = [np.arange(int(cu[j]) + b, int(cu[j + 1])) for j, b in enumerate(starts)]
+    idx = np.concatenate(rows)
+    xs = wl.Inputs(x.q[idx], x.k[idx], x.v[idx], x.g[idx], x.beta[idx],
+                   np.concatenate([[0], np.cumsum([len(r) for r in rows])]).astype(np.int32), x.io_dtype)
+    state = torch.zeros((len(lens), H, 128, 128), dtype=torch.float32, device="cuda")
+    for j, b in enumerate(starts):
+        if b > 0:
+            state[j] = res.ckpt[int(res.ckpt_offsets[j]) + b // C - 1]
+    r2 = api.prefill_resume(api.to_device(xs), starts, state, C)
+    torch.cuda.synchronize()
+    assert torch.equal(r2.o, res.o[torch.from_numpy(idx).cuda()])
+    assert torch.equal(r2.final_state, res.final_state)
