@@ -40,9 +40,15 @@ template <typename T, int DK> struct GroupOps {
     static constexpr int VU = kChunk / 4 / VEC;           // K~^T vectors per row tile
     static constexpr int NW = 4 * VS;                     // -W vectors per chunk
     static constexpr int NV = NW + (DK / 16) * VU;        // all vectors (1 KB each)
-    static constexpr int PER_WAVE = NV / kGroupWaves;
-    static_assert(NW == (DK / 16) * VU && PER_WAVE * kGroupWaves == NV, "operand split");
+    static_assert(NW == (DK / 16) * VU, "operand split");
 };
+
+// Scan waves of a workgroup: the maps of a 128 x 128 state (16 column tiles
+// of [Phi | R]) run on 8 waves of 2 tiles, so every wave streams its
+// fragments with 2 tiles' state in registers; the other forms on 4.
+template <int DK, int DV, int MODE> constexpr int group_scan_waves() {
+    return (MODE == kGroupTrans && (DK / 16) % 8 == 0 && ((DK + DV) / 16) % 8 == 0) ? 8 : kGroupWaves;
+}
 
 // LDS of the output waves (OUT): the handoff of one chunk, i.e. the state
 // entering it and U of every column tile in the MFMA operand order the scan
@@ -58,27 +64,27 @@ template <typename T, int DK, int DV> struct GroupOutLds {
 };
 
 template <typename T, int DK, int DV, int MODE, bool OUT = false>
-__global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_kernel(ScanArgs a) {
+__global__ __launch_bounds__((64 * group_scan_waves<DK, DV, MODE>() * (OUT ? 2 : 1))) void gdr_group_kernel(ScanArgs a) {
     using M = MT<T>;
     using L = WsLayout<T, DK, DV>;
     using G = GroupOps<T, DK>;
-    constexpr int KW = M::KW, VEC = G::VEC, VS = G::VS, VU = G::VU, NV = G::NV, PW = G::PER_WAVE;
+    constexpr int NSW = group_scan_waves<DK, DV, MODE>();                  // scan waves
+    constexpr int KW = M::KW, VEC = G::VEC, VS = G::VS, VU = G::VU, NV = G::NV, PW = NV / NSW;
     constexpr int RT = DK / 16, FS = DK / 4, FU = kChunk / 4;
     constexpr int NTU = (MODE == kGroupTrans) ? (DK + DV) / 16 : DV / 16;   // tiles per unit
-    constexpr int TPW = NTU / kGroupWaves;
-    constexpr int NPHI = (MODE == kGroupTrans) ? DK / 64 : 0;               // Phi tiles per wave
+    constexpr int TPW = NTU / NSW;
+    constexpr int NPHI = (MODE == kGroupTrans) ? DK / 16 / NSW : 0;         // Phi tiles per wave
     constexpr bool kHandOff = MODE != kGroupTrans;
-    constexpr bool kStream = MODE != kGroupTrans;       // fragments streamed a few ahead of their MFMAs
     constexpr bool kScan = MODE == kGroupScan;
-    static_assert(TPW * kGroupWaves == NTU, "tiles per wave");
-    static_assert(!kStream || (VEC == KW && sizeof(T) == 2), "streamed step: bf16 fragments, one k-step each");
-    static_assert(!OUT || kStream, "output waves serve the replay and scan forms");
-    constexpr int kMfmas = TPW * (4 * VS + RT * VU) * (VEC / KW);     // per chunk
+    static_assert(TPW * NSW == NTU && PW * NSW == NV, "tiles and operand vectors per wave");
+    static_assert(MODE != kGroupTrans || NPHI * NSW == DK / 16, "Phi tiles per wave");
+    static_assert(VEC == KW && sizeof(T) == 2, "streamed step: bf16 fragments, one k-step each");
+    static_assert(!OUT || NSW == kGroupWaves, "output waves pair with 4 scan waves");
     constexpr int kLoads = PW + 1 + 4 * (TPW - NPHI) + (kScan ? 1 : 0);   // global loads per chunk
 
     __shared__ uint4 ops_lds[2][NV][64];
-    // With OUT, waves kGroupWaves .. 2 kGroupWaves - 1 are output waves: wave
-    // kGroupWaves + w reads out scan wave w's tiles.  Per chunk j all waves
+    // With OUT, waves NSW .. 2 NSW - 1 are output waves: wave
+    // NSW + w reads out scan wave w's tiles.  Per chunk j all waves
     // pass two barriers: A_j (the scan waves have written chunk j's handoff)
     // and B_j (the output waves have read it, so chunk j+1's may be
     // written).  The output waves compute chunk j's output while the scan
@@ -116,16 +122,16 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
     const int n = c1 - c0;
 
     if constexpr (OUT) {
-        if (w >= kGroupWaves) {
+        if (w >= NSW) {
             // Output wave.  It stages its quarter of every chunk's Q and P
             // fragments into the ring one chunk ahead, and computes
             //   O^T = scale ((S_0^T Q^T) diag(exp G) + U^T P^T)
             // for its tiles with each fragment read from LDS once for all of
             // them, in the same MFMA order as the split output kernel (so the
             // two give identical bits).
-            constexpr int NQ = OL::NQ, NQP = OL::NQP, QPW = NQP / kGroupWaves;
-            static_assert(QPW * kGroupWaves == NQP, "Q/P split");
-            const int wo = w - kGroupWaves;
+            constexpr int NQ = OL::NQ, NQP = OL::NQP, QPW = NQP / NSW;
+            static_assert(QPW * NSW == NQP, "Q/P split");
+            const int wo = w - NSW;
             const int64_t cu0 = a.cu[seq];
             const uint32_t l16 = 16u * (uint32_t)lane;
             auto load_qp = [&](uint4 (&r)[QPW], uint4 &eg, int jj) {
@@ -151,7 +157,7 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
                 T sb[TPW][FS], ub[TPW][FU];
 #pragma unroll
                 for (int i = 0; i < TPW; ++i) {
-                    const int tile = i * kGroupWaves + wo;
+                    const int tile = i * NSW + wo;
 #pragma unroll
                     for (int v = 0; v < VS; ++v) *(uint4 *)&sb[i][v * VEC] = hand[0].sb[tile][v][lane];
 #pragma unroll
@@ -189,7 +195,7 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
                         T out[4];
 #pragma unroll
                         for (int e4 = 0; e4 < 4; ++e4) out[e4] = from_f32<T>(acc[i][e4] * a.scale);
-                        const int tile = i * kGroupWaves + wo;
+                        const int tile = i * NSW + wo;
                         const uint32_t voff = ((uint32_t)(16 * mt + c16) * (uint32_t)(H * DV) +
                                                (uint32_t)(16 * tile + 4 * g16)) * (uint32_t)sizeof(T);
                         buf_store_4<T>(ro, voff, out);
@@ -224,7 +230,7 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
     f32x4 S[TPW][RT];
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
-        const int tile = i * kGroupWaves + w;
+        const int tile = i * NSW + w;
         if (MODE == kGroupTrans && i < NPHI) {
             const int col = 16 * tile + c16;
 #pragma unroll
@@ -251,7 +257,7 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
     ChunkCursor cur{0, a.C, len, a.C};
     if constexpr (kScan) ck.init(a, seq, h, len, (size_t)DK * DV, w == 0);
     auto lane_off = [&](int i) {
-        return 4u * (uint32_t)(4 * g16 * DV + 16 * (i * kGroupWaves + w) + c16);
+        return 4u * (uint32_t)(4 * g16 * DV + 16 * (i * NSW + w) + c16);
     };
     auto store_state = [&](float *d) {
 #pragma unroll
@@ -260,7 +266,7 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
     __builtin_amdgcn_s_waitcnt(0);
 
     // this wave's quarter of the chunk operands: -W (waves 0, 1) or K~^T (2, 3)
-    const bool loads_w = w < kGroupWaves / 2;
+    const bool loads_w = w < NSW / 2;
     const int vbase = w * PW;                                  // first vector (LDS index)
     const int vsrc = loads_w ? vbase : vbase - G::NW;          // within its region
     auto load_slice = [&](uint4 (&r)[PW], int jj) {
@@ -284,7 +290,7 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
         const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
 #pragma unroll
         for (int i = NPHI; i < TPW; ++i) {
-            const int ut_tile = i * kGroupWaves + w - (MODE == kGroupTrans ? DK / 16 : 0);
+            const int ut_tile = i * NSW + w - (MODE == kGroupTrans ? DK / 16 : 0);
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
                 const uint4 x = buf_load16(ru, lane16, 1024u * (ut_tile * 4 + mt));
@@ -298,92 +304,8 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
         for (int v = 0; v < PW; ++v) ops_lds[buf][vbase + v][lane] = r[v];
     };
 
-    // Whole-chunk form (maps): every fragment read from LDS up front.
-    auto step_all = [&](const Own &o, int buf, int jj) {
-        const int64_t sh = (base + c0 + jj) * H + h;
-        uint4 wf[G::NW], kf[NV - G::NW];
-#pragma unroll
-        for (int v = 0; v < G::NW; ++v) wf[v] = ops_lds[buf][v][lane];
-#pragma unroll
-        for (int v = 0; v < NV - G::NW; ++v) kf[v] = ops_lds[buf][G::NW + v][lane];
-        T sb[TPW][FS];
-#pragma unroll
-        for (int i = 0; i < TPW; ++i)
-#pragma unroll
-            for (int f = 0; f < FS; ++f) sb[i][f] = from_f32<T>(S[i][f >> 2][f & 3]);
-        if constexpr (kHandOff) {
-            const auto rs = make_rsrc((T *)a.ws.sc + sh * L::sc_elems, L::sc_elems * sizeof(T));
-#pragma unroll
-            for (int i = 0; i < TPW; ++i)
-#pragma unroll
-                for (int v = 0; v < VS; ++v)
-                    buf_store16(*(const uint4 *)&sb[i][v * VEC], rs, lane16, 1024u * ((i * kGroupWaves + w) * VS + v));
-        }
-        // U = U~ - W S for every tile; each -W fragment read once
-        f32x4 U[TPW][4];
-#pragma unroll
-        for (int i = 0; i < TPW; ++i)
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                if (i < NPHI) U[i][mt] = zero4();
-                else U[i][mt] = o.ut[i - NPHI][mt];
-            }
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-            for (int v = 0; v < VS; ++v) {
-                const T *fv = (const T *)&wf[mt * VS + v];
-#pragma unroll
-                for (int kk = 0; kk < VEC / KW; ++kk)
-#pragma unroll
-                    for (int i = 0; i < TPW; ++i)
-                        U[i][mt] = M::mma(M::pack(&fv[kk * KW]), M::pack(&sb[i][v * VEC + kk * KW]), U[i][mt]);
-            }
-        T ub[TPW][FU];
-#pragma unroll
-        for (int i = 0; i < TPW; ++i)
-#pragma unroll
-            for (int f = 0; f < FU; ++f) ub[i][f] = from_f32<T>(U[i][f >> 2][f & 3]);
-        if constexpr (kHandOff) {
-            const auto rs = make_rsrc((T *)a.ws.u + sh * L::u_elems, L::u_elems * sizeof(T));
-#pragma unroll
-            for (int i = 0; i < TPW; ++i)
-#pragma unroll
-                for (int v = 0; v < VU; ++v)
-                    buf_store16(*(const uint4 *)&ub[i][v * VEC], rs, lane16, 1024u * ((i * kGroupWaves + w) * VU + v));
-        }
-        // S = exp(G_63) S + K~^T U; each K~^T fragment read once
-        const float decay = expf(o.gl);
-        if constexpr (MODE == kGroupTrans) dprod *= decay;
-#pragma unroll
-        for (int i = 0; i < TPW; ++i)
-#pragma unroll
-            for (int t = 0; t < RT; ++t) S[i][t] = S[i][t] * decay;
-#pragma unroll
-        for (int t = 0; t < RT; ++t)
-#pragma unroll
-            for (int v = 0; v < VU; ++v) {
-                const T *fv = (const T *)&kf[t * VU + v];
-#pragma unroll
-                for (int kk = 0; kk < VEC / KW; ++kk)
-#pragma unroll
-                    for (int i = 0; i < TPW; ++i)
-                        S[i][t] = M::mma(M::pack(&fv[kk * KW]), M::pack(&ub[i][v * VEC + kk * KW]), S[i][t]);
-            }
-        // Issue order in this region: this wave's LDS writes of the next
-        // chunk, every fragment read, then the MFMAs with the global loads
-        // (next chunk's slice and per-tile operands) one per MFMA.
-        __builtin_amdgcn_sched_group_barrier(0x200, PW, 0);   // LDS writes
-        __builtin_amdgcn_sched_group_barrier(0x100, NV, 0);   // LDS reads
-#pragma unroll
-        for (int q = 0; q < kMfmas; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                   // MFMA
-            if (q < kLoads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
-        }
-    };
-
-    // Streamed form (replay, scan): the chunk's NV fragments are read from
-    // LDS kAhead ahead of the TPW MFMAs each feeds.  The U phase walks the -W
+    // Streamed step: the chunk's NV fragments are read from LDS kAhead
+    // ahead of the TPW MFMAs each feeds.  The U phase walks the -W
     // fragments dk-step-major (fragment f = 4 v + mt is row tile mt, dk step
     // v), so the state's bf16 operand of dk step v is formed just before its
     // four fragments; every accumulator still sums its dk steps in order, as
@@ -400,7 +322,7 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
 #pragma unroll
         for (int i = 0; i < TPW; ++i)
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt) U[i][mt] = o.ut[i][mt];
+            for (int mt = 0; mt < 4; ++mt) U[i][mt] = i < NPHI ? zero4() : o.ut[i - NPHI][mt];   // Phi tiles take no U~
         const auto rsc = make_rsrc((T *)a.ws.sc + sh * L::sc_elems, L::sc_elems * sizeof(T));
 #pragma unroll
         for (int v = 0; v < VS; ++v) {
@@ -410,10 +332,10 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
 #pragma unroll
                 for (int e = 0; e < 8; ++e) sv[i][e] = from_f32<T>(S[i][2 * v + (e >> 2)][e & 3]);
                 if constexpr (OUT)
-                    hand[0].sb[i * kGroupWaves + w][v][lane] = __builtin_bit_cast(uint4, sv[i]);
-                else
+                    hand[0].sb[i * NSW + w][v][lane] = __builtin_bit_cast(uint4, sv[i]);
+                else if constexpr (kHandOff)
                     buf_store16(__builtin_bit_cast(uint4, sv[i]), rsc, lane16,
-                                1024u * ((i * kGroupWaves + w) * VS + v));
+                                1024u * ((i * NSW + w) * VS + v));
             }
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
@@ -433,13 +355,14 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
 #pragma unroll
                 for (int e = 0; e < 8; ++e) ub[i][v][e] = from_f32<T>(U[i][2 * v + (e >> 2)][e & 3]);
                 if constexpr (OUT)
-                    hand[0].ub[i * kGroupWaves + w][v][lane] = __builtin_bit_cast(uint4, ub[i][v]);
-                else
+                    hand[0].ub[i * NSW + w][v][lane] = __builtin_bit_cast(uint4, ub[i][v]);
+                else if constexpr (kHandOff)
                     buf_store16(__builtin_bit_cast(uint4, ub[i][v]), ru, lane16,
-                                1024u * ((i * kGroupWaves + w) * VU + v));
+                                1024u * ((i * NSW + w) * VU + v));
             }
         // S = exp(G_63) S + K~^T U
         const float decay = expf(o.gl);
+        if constexpr (MODE == kGroupTrans) dprod *= decay;
 #pragma unroll
         for (int i = 0; i < TPW; ++i)
 #pragma unroll
@@ -471,10 +394,7 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
             }
         }
     };
-    auto step = [&](const Own &o, int buf, int jj) {
-        if constexpr (kStream) step_stream(o, buf, jj);
-        else step_all(o, buf, jj);
-    };
+    auto step = [&](const Own &o, int buf, int jj) { step_stream(o, buf, jj); };
     // After chunk jj's barrier (scan form): its checkpoint, if it ends on a
     // multiple of C.  S still holds the state after chunk jj.
     auto after = [&](int ckid) {
@@ -536,7 +456,7 @@ __global__ __launch_bounds__(64 * kGroupWaves * (OUT ? 2 : 1)) void gdr_group_ke
         const int64_t ssh = seg_slot * H + h;
 #pragma unroll
         for (int i = 0; i < TPW; ++i) {
-            const int tile = i * kGroupWaves + w;
+            const int tile = i * NSW + w;
             if (i < NPHI) {
                 const int col = 16 * tile + c16;
                 T *dst = (T *)a.seg.phi + ssh * DK * DK + phi_col_pos(col);

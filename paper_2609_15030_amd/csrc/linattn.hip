@@ -248,7 +248,7 @@ la_status launch_two_level(const PrefillCall &c, const WsPlan &p, la::ScanArgs s
     const int64_t units = pairs * sa.max_seg;
     if (units > 0) {
         hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupTrans>), dim3((unsigned)units),
-                           dim3(64 * la::kGroupWaves), 0, c.stream, sa);
+                           dim3(64 * la::group_scan_waves<DK, DV, la::kGroupTrans>()), 0, c.stream, sa);
         if (la_status e = hip_check("segment map launch")) return e;
     }
     hipLaunchKernelGGL((la::gdr_seg_combine_kernel<T, DK, DV>), dim3((unsigned)(8 * NT * ((pairs + 7) / 8))),
