@@ -287,16 +287,12 @@ __global__ __launch_bounds__((64 * group_scan_waves<DK, DV, MODE>() * (OUT ? 2 :
         const int64_t sh = (base + c0 + jj) * H + h;
         o.gl = buf_load4f(make_rsrc(a.ws.g + sh * kChunk, kChunk * sizeof(float)), 0u, 4u * (kChunk - 1));
         o.ckid = kScan ? ck.load_id(jj / a.cps) : 0;
-        const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
+        const auto ru = make_rsrc((const T *)a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(T));
 #pragma unroll
         for (int i = NPHI; i < TPW; ++i) {
             const int ut_tile = i * NSW + w - (MODE == kGroupTrans ? DK / 16 : 0);
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                const uint4 x = buf_load16(ru, lane16, 1024u * (ut_tile * 4 + mt));
-                o.ut[i - NPHI][mt] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z),
-                                           __uint_as_float(x.w)};
-            }
+            for (int mt = 0; mt < 4; ++mt) o.ut[i - NPHI][mt] = load_ut<T>(ru, (uint32_t)lane, (uint32_t)(ut_tile * 4 + mt));
         }
     };
     auto store_slice = [&](const uint4 (&r)[PW], int buf) {

@@ -370,14 +370,20 @@ __global__ __launch_bounds__(256, sizeof(PrepSmem<T, DK, DV>) <= 80 * 1024 ? 2 :
             for (int v = 0; v < NV; ++v)
                 *(uint4 *)(wout + ((size_t)(mt * NV + v) * 64 + lane) * VEC) = *(const uint4 *)&wf[v * VEC];
         }
-        float4 *ut = (float4 *)(a.ws.ut + sh * WsLayout<T, DK, DV>::ut_elems);
+        T *ut = (T *)a.ws.ut + sh * WsLayout<T, DK, DV>::ut_elems;
 #pragma unroll
         for (int nt = 0; nt < DV / 16; ++nt) {
             f32x4 acc = zero4();
 #pragma unroll
             for (int ks = 0; ks < NKS; ++ks)
                 acc = M::mma(f2[ks], RT::bfrag(&sm.vs[0][0], LDV, ks * KSTEP, 16 * nt, lane), acc);
-            ut[(nt * 4 + mt) * 64 + lane] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+            T u4[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) u4[i] = from_f32<T>(acc[i]);
+            if constexpr (sizeof(T) == 4)
+                *(uint4 *)(ut + ((size_t)(nt * 4 + mt) * 64 + lane) * 4) = *(const uint4 *)u4;
+            else
+                *(uint2 *)(ut + ((size_t)(nt * 4 + mt) * 64 + lane) * 4) = *(const uint2 *)u4;
         }
         // K~^T: per dk row tile, lane holds 16 values at chunk rows perm_row(f, g)
         T *kout = (T *)a.ws.kt + sh * WsLayout<T, DK, DV>::kt_elems;

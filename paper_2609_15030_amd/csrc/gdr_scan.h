@@ -340,12 +340,9 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_scan_kernel(ScanArgs a) {
         // use waits only for the loads issued before it)
         o.gl = buf_load4f(make_rsrc(a.ws.g + sh * kChunk, kChunk * sizeof(float)), 0u, 4u * (kChunk - 1));
         o.ckid = ck.load_id(jj / a.cps);
-        const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
+        const auto ru = make_rsrc((const T *)a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(T));
 #pragma unroll
-        for (int m = 0; m < MTW; ++m) {
-            const uint4 x = buf_load16(ru, lane16, 1024u * (tile * 4 + w * MTW + m));
-            o.ut[m] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
-        }
+        for (int m = 0; m < MTW; ++m) o.ut[m] = load_ut<T>(ru, (uint32_t)lane, (uint32_t)(tile * 4 + w * MTW + m));
         const auto rw = make_rsrc((const T *)a.ws.w + sh * L::w_elems, L::w_elems * sizeof(T));
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt)
@@ -501,12 +498,9 @@ __device__ inline void scan1_chunks(const ScanArgs &a, int seq, int h, int tile,
         const int64_t sh = (base + jj) * H + h;
         o.gl = buf_load4f(make_rsrc(a.ws.g + sh * kChunk, kChunk * sizeof(float)), 0u, 4u * (kChunk - 1));
         o.ckid = ck.load_id(jj / a.cps);
-        const auto ru = make_rsrc(a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(float));
+        const auto ru = make_rsrc((const T *)a.ws.ut + sh * L::ut_elems, L::ut_elems * sizeof(T));
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            const uint4 x = buf_load16(ru, lane16 + 1024u * (tile * 4 + mt), 0u);
-            o.ut[mt] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
-        }
+        for (int mt = 0; mt < 4; ++mt) o.ut[mt] = load_ut<T>(ru, (uint32_t)lane, (uint32_t)(tile * 4 + mt));
         const auto rw = make_rsrc((const T *)a.ws.w + sh * L::w_elems, L::w_elems * sizeof(T));
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt)

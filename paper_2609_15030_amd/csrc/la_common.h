@@ -209,7 +209,7 @@ __host__ inline int64_t chunk_grid_blocks(int n_seqs, int n_heads, int64_t max_c
 // device within one prefill call.
 //   W   : -W in A-operand order for the state contraction      [4][DK/4] x 64 lanes, io type
 //   KT  : decayed keys^T in A-operand order (chunk rows perm.) [DK/16][16] x 64 lanes, io type
-//   UT  : U~ = T diag(beta) V, C-layout per 16x16 tile        [DV/16][4] x 64 lanes x 4, fp32
+//   UT  : U~ = T diag(beta) V, C-layout per 16x16 tile        [DV/16][4] x 64 lanes x 4, io type
 //   G   : chunk-local cumulative gate, row 16 m + c at 4 c + m [64], fp32
 //         (a lane's four output rows in one 16-byte load; row 63 stays at 63)
 //   SC  : state entering the chunk, B-operand order            [DV/16][DK/4] x 64 lanes, io type
@@ -220,9 +220,25 @@ __host__ inline int64_t chunk_grid_blocks(int n_seqs, int n_heads, int64_t max_c
 //                                                              [4][DK/4] x 64 lanes, io type
 // ---------------------------------------------------------------------------
 struct Workspace {
-    void *w, *kt, *sc, *u, *p, *qf;
-    float *ut, *g;
+    void *w, *kt, *sc, *u, *p, *qf, *ut;
+    float *g;
 };
+
+// U~ tile vector `vec` (= column tile * 4 + row tile) of one slot-head, as
+// lane `lane` holds it in the C layout (rows 4 (lane / 16) + i, column
+// lane % 16): four consecutive elements of the io type, widened to fp32 as
+// the accumulator of U = U~ - W S.
+template <typename T>
+__device__ inline f32x4 load_ut(__amdgpu_buffer_rsrc_t r, uint32_t lane, uint32_t vec) {
+    if constexpr (sizeof(T) == 4) {
+        const uint4 x = buf_load16(r, 16u * lane, 1024u * vec);
+        return f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
+    } else {
+        const uint2 x = buf_load8(r, 8u * lane, 512u * vec);
+        return f32x4{__uint_as_float(x.x << 16), __uint_as_float(x.x & 0xffff0000u), __uint_as_float(x.y << 16),
+                     __uint_as_float(x.y & 0xffff0000u)};
+    }
+}
 
 template <typename T, int DK, int DV> struct WsLayout {
     static constexpr size_t w_elems = (size_t)kChunk * DK;      // per slot-head

@@ -176,7 +176,7 @@ WsPlan plan_workspace(const la_shape *s, int64_t total_tokens) {
     auto take = [&](size_t bytes) { const size_t at = off; off = round_up(off + bytes, kRegionAlign); return at; };
     p.w = take(sh * la::kChunk * s->dk * io);
     p.kt = take(sh * s->dk * la::kChunk * io);
-    p.ut = take(sh * la::kChunk * s->dv * sizeof(float));
+    p.ut = take(sh * la::kChunk * s->dv * io);
     p.g = take(sh * la::kChunk * sizeof(float));
     p.sc = take(sh * (size_t)s->dk * s->dv * io);
     p.u = take(sh * la::kChunk * s->dv * io);
@@ -299,7 +299,7 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
     la::Workspace ws;
     ws.w = base + p.w;
     ws.kt = base + p.kt;
-    ws.ut = (float *)(base + p.ut);
+    ws.ut = base + p.ut;
     ws.g = (float *)(base + p.g);
     ws.sc = base + p.sc;
     ws.u = base + p.u;
