@@ -15,6 +15,7 @@
 #include "gdr_prep.h"
 #include "gdr_scan.h"
 #include "gdr_group.h"
+#include "gdr_scan_pair.h"
 #include "gdr_out.h"
 #include "gdr_decode.h"
 #include "paged.h"
@@ -98,6 +99,49 @@ bool scan_with_output(int64_t blocks) {
     }
     const int64_t rounds = sizeof(T) == 2 ? 2 : 1;
     return blocks <= rounds * capacity[dev];
+}
+
+// Workgroups of `kernel` (launched with `threads` lanes) resident on the
+// current device at once; cached per device and caller slot.  0 when the
+// runtime cannot say.
+template <typename K>
+int64_t resident_capacity(K kernel, int threads, int slot) {
+    static int64_t cache[4][64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64 || slot < 0 || slot >= 4) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    if (cache[slot][dev] == 0) {
+        int per_cu = 0, cus = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+            (void)hipGetLastError();
+            return 0;
+        }
+        cache[slot][dev] = (int64_t)per_cu * cus;
+    }
+    return cache[slot][dev];
+}
+
+// Whether a bf16 call with the scan and output stages runs the scan with
+// output wave over pairs of column tiles (gdr_scan2o_kernel) instead of one
+// tile per workgroup: when the one-tile workgroups do not all fit at once
+// but the pair workgroups fit in two rounds.  Several scan workgroups then
+// share each CU, whose load path bounds their chunk steps, and a pair moves
+// half the operand bytes per tile (16-sequence, 8-head varlen batch:
+// 1,024 one-tile or 512 pair workgroups).  LA_SCAN_PAIR=1|0 forces the
+// choice (for measurement).
+template <typename T, int DK, int DV>
+bool scan_by_pairs(int64_t blocks1, int64_t blocks2) {
+    static const int forced = [] {
+        const char *e = getenv("LA_SCAN_PAIR");
+        return e ? atoi(e) : -1;
+    }();
+    if (forced == 0 || forced == 1) return forced == 1;
+    const int64_t cap1 = resident_capacity(la::gdr_scan1o_kernel<T, DK, DV>, 128, 0);
+    const int64_t cap2 = resident_capacity(la::gdr_scan2o_kernel<T, DK, DV>, 128, 1);
+    return cap1 > 0 && cap2 > 0 && blocks1 > cap1 && blocks2 <= 2 * cap2;
 }
 
 // Whether a single-level bf16 scan runs as one workgroup per (sequence,
@@ -337,6 +381,15 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
             if (p.seg_m > 1) return launch_two_level<T, DK, DV>(c, p, sa, max_chunks, trace);
         }
         const bool out_stage = (c.stages & LA_STAGE_OUTPUT) != 0;
+        if constexpr (sizeof(T) == 2) {
+            const int64_t blocks2 = 8 * (NT / la::kPairTiles) * ((pairs + 7) / 8);
+            if (out_stage && scan_variant(false, DK) == 1 && scan_by_pairs<T, DK, DV>(blocks, blocks2)) {
+                hipLaunchKernelGGL((la::gdr_scan2o_kernel<T, DK, DV>), dim3((unsigned)blocks2), dim3(128), 0,
+                                   c.stream, sa);
+                if (la_status e = hip_check("inter-chunk scan launch")) return e;
+                return launch_out<T, DK, DV>(c, ws, 0, trace);
+            }
+        }
         const bool with_out = scan_variant(sizeof(T) == 4, DK) == 1 && out_stage && scan_with_output<T, DK, DV>(blocks);
         if constexpr (sizeof(T) == 2) {
             if (scan_by_group(with_out, out_stage)) {
