@@ -68,9 +68,19 @@ __device__ inline uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint
     return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
 }
 
+// 16 bytes as two 8-byte buffer stores.  A buffer store of more than 8
+// bytes reads its data registers after issue: an instruction right behind
+// it that rewrites them corrupts the stored words, and the compiler does not
+// separate the two when the store's offset sits in a scalar register (the
+// form every store here takes).  Stores of 8 bytes or less are free of that
+// hazard.  The empty asm statement between the halves keeps the compiler
+// from merging them back into one 16-byte store.
 __device__ inline void buf_store16(uint4 x, __amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-    const i32x4 v = {(int)x.x, (int)x.y, (int)x.z, (int)x.w};
-    __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, (int)soff, 0);
+    typedef int i32x2 __attribute__((ext_vector_type(2)));
+    const i32x2 lo = {(int)x.x, (int)x.y}, hi = {(int)x.z, (int)x.w};
+    __builtin_amdgcn_raw_buffer_store_b64(lo, r, (int)voff, (int)soff, 0);
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_raw_buffer_store_b64(hi, r, (int)(voff + 8u), (int)soff, 0);
 }
 
 __device__ inline uint2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {

@@ -74,13 +74,17 @@ size_t io_size(int32_t dtype) { return dtype == LA_BF16 ? 2 : 4; }
 // both the split kernels, whose state and U make a round trip through HBM,
 // and the workgroup scan, bound by its CU's LDS bandwidth).
 // LA_SCAN_OUTPUT=0 selects the split kernels (for measurement).
-template <typename T, int DK, int DV>
-bool scan_with_output(int64_t blocks) {
+bool output_waves_on() {
     static const bool on = [] {
         const char *e = getenv("LA_SCAN_OUTPUT");
         return !(e && atoi(e) == 0);
     }();
-    if (!on) return false;
+    return on;
+}
+
+template <typename T, int DK, int DV>
+bool scan_with_output(int64_t blocks) {
+    if (!output_waves_on()) return false;
     static int64_t capacity[64] = {};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
@@ -139,6 +143,7 @@ bool scan_by_pairs(int64_t blocks1, int64_t blocks2) {
         return e ? atoi(e) : -1;
     }();
     if (forced == 0 || forced == 1) return forced == 1;
+    if (!output_waves_on()) return false;
     const int64_t cap1 = resident_capacity(la::gdr_scan1o_kernel<T, DK, DV>, 128, 0);
     const int64_t cap2 = resident_capacity(la::gdr_scan2o_kernel<T, DK, DV>, 128, 1);
     return cap1 > 0 && cap2 > 0 && blocks1 > cap1 && blocks2 <= 2 * cap2;
@@ -157,7 +162,7 @@ bool scan_by_group(bool tile_scan_with_output, bool output_stage) {
         return e ? atoi(e) : -1;
     }();
     if (forced == 0 || forced == 1) return forced == 1;
-    return output_stage && !tile_scan_with_output;
+    return output_stage && !tile_scan_with_output && output_waves_on();
 }
 
 // Chunks per segment of the two-level scan (1 = single-level).  A segment
@@ -301,7 +306,7 @@ la_status launch_two_level(const PrefillCall &c, const WsPlan &p, la::ScanArgs s
     // the replay's output waves produce the output when the call includes
     // the output stage; otherwise the split output kernel reads the states
     // and U the replay leaves in the workspace
-    const bool out_stage = (c.stages & LA_STAGE_OUTPUT) != 0;
+    const bool out_stage = (c.stages & LA_STAGE_OUTPUT) != 0 && output_waves_on();
     if (units > 0) {
         if (out_stage)
             hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupReplay, true>), dim3((unsigned)units),
@@ -392,7 +397,9 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
         }
         const bool with_out = scan_variant(sizeof(T) == 4, DK) == 1 && out_stage && scan_with_output<T, DK, DV>(blocks);
         if constexpr (sizeof(T) == 2) {
-            if (scan_by_group(with_out, out_stage)) {
+            // the workgroup scan stands in for the single-wave form only (the
+            // dk-split scan sums its partial products in another order)
+            if (scan_variant(false, DK) == 1 && scan_by_group(with_out, out_stage)) {
                 // one workgroup per (sequence, head) chain: 4 scan waves, and
                 // 4 output waves when the call includes the output stage
                 sa.seg_m = 1;

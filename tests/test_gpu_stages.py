@@ -91,3 +91,23 @@ def test_scan_output_wave_equals_split_output_kernel(dk, dv, io):
     torch.cuda.synchronize()
     res = api.PrefillResult(p.o, p.final, p.ckpt, p.ckpt_offsets, p.n_ckpt_rows)
     assert _equal(ref, res)
+
+
+def test_split_handoff_exact_at_batch_scale():
+    """The scan stage on its own hands the state entering every chunk and U
+    to the output stage through the workspace (16-byte words per lane).
+    Regression: a store-data hazard once left a few of those words wrong on
+    some runs (about 1 KiB in a 700 MiB workspace), so small batches rarely
+    showed it.  Three stage-split runs of the 16-sequence varlen batch must
+    equal the one-call result bit for bit."""
+    w = wl.batched_varlen()
+    xd = api.to_device(w.inputs)
+    ref = api.Prefill(xd, w.interval).run()
+    ref_o, ref_f, ref_c = ref.o.clone(), ref.final_state.clone(), ref.ckpt.clone()
+    p = api.Prefill(xd, w.interval)
+    for _ in range(3):
+        p.run(stages=P)
+        p.run(stages=S)
+        p.run(stages=O)
+        torch.cuda.synchronize()
+        assert torch.equal(p.o, ref_o) and torch.equal(p.final, ref_f) and torch.equal(p.ckpt, ref_c)
