@@ -232,3 +232,23 @@ def test_many_chains_workgroup_scan():
     torch.cuda.synchronize()
     assert torch.equal(r2.o, res.o[torch.from_numpy(idx).cuda()])
     assert torch.equal(r2.final_state, res.final_state)
+
+
+@pytest.mark.parametrize("dk,dv", [(64, 64), (64, 128), (128, 64)])
+def test_pair_tile_scan_head_dims(dk, dv):
+    """33 sequences x 8 heads: more one-tile scan workgroups than are
+    resident at once, so the scan with output wave runs over pairs of column
+    tiles.  Parity with the oracle, and a sequence alone (one-tile kernel)
+    gives the same bits as inside the batch."""
+    rng = np.random.default_rng(600 + dk + dv)
+    lens = [int(n) for n in rng.integers(64, 700, size=33)]
+    C = 128
+    x = wl.random_inputs(600 + dk + dv, lens, 8, dk, dv, wl.BF16)
+    xd, res = _run_cold(x, C)
+    ref = oracle_run(x, interval=C)
+    compare(res, ref, x.cu_seqlens, TOL[la.LA_BF16], f"33 seqs x 8 heads dk={dk} dv={dv}, pair-tile scan")
+    i = int(np.argmax(lens))
+    alone = api.prefill(api.to_device(x.seq(i)), C)
+    torch.cuda.synchronize()
+    s, e = int(x.cu_seqlens[i]), int(x.cu_seqlens[i + 1])
+    assert torch.equal(alone.o, res.o[s:e]) and torch.equal(alone.final_state[0], res.final_state[i])
