@@ -312,15 +312,16 @@ def bench_hybrid(la, torch, stream_ptr, events, n_tokens, interval, n_heads, pag
         for _ in range(3):
             la.la_hybrid_restore(kv, bdev, [B], stp, sid, states, n_heads)
         torch.cuda.synchronize()
-        # back-to-back launches: the entry point's host-side checks of the pools
-        # overlap the previous launch instead of idling the GPU between events
-        # (one more launch queued first, so the GPU is busy at the start event)
-        la.la_hybrid_restore(kv, bdev, [B], stp, sid, states, n_heads)
-        events.record(4, stream_ptr)
-        for _ in range(reps):
+        # one event pair per launch: the entry point's host-side checks of the
+        # pools take about as long as a device-pool restore, so an interval
+        # over back-to-back launches would hold host time whenever the GPU
+        # waits for the next launch
+        ev = HipEvents(2 * reps)
+        for r in range(reps):
+            ev.record(2 * r, stream_ptr)
             la.la_hybrid_restore(kv, bdev, [B], stp, sid, states, n_heads)
-        events.record(5, stream_ptr)
-        us = events.ms(4, 5) / reps * 1e3
+            ev.record(2 * r + 1, stream_ptr)
+        us = sum(ev.ms(2 * r, 2 * r + 1) for r in range(reps)) / reps * 1e3
         gbps = payload / (us * 1e-6) / 1e9
         out[name] = {"us": round(us, 2), "payload_GBps": round(gbps, 1)}
         if name == "device_pool":
