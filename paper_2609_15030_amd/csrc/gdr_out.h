@@ -117,6 +117,7 @@ struct OutArgs {
     int32_t n_seqs, n_heads, C, cps, max_chunks;
     float scale;
     Workspace ws;
+    int32_t chunk_major;   // block map (see unit_of_block)
 };
 
 // Split output kernel (used when the scan ran without its output wave: the
@@ -132,7 +133,7 @@ __global__ __launch_bounds__(4 * DV) void gdr_out_kernel(OutArgs a) {
     const int lane = threadIdx.x & 63, tile = threadIdx.x >> 6;
     int64_t j;
     int seq, h;
-    if (!unit_of_block(a.n_seqs, a.n_heads, a.max_chunks, &seq, &h, &j)) return;
+    if (!unit_of_block(a.n_seqs, a.n_heads, a.max_chunks, a.chunk_major != 0, &seq, &h, &j)) return;
     const int H = a.n_heads;
     const int64_t cu0 = a.cu[seq];
     const int len = a.cu[seq + 1] - a.cu[seq];

@@ -36,6 +36,7 @@ struct PrepArgs {
     const int32_t *cu;
     int32_t n_seqs, n_heads, C, cps, variant, max_chunks;
     Workspace ws;
+    int32_t chunk_major;   // block map (see unit_of_block)
 };
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -159,7 +160,7 @@ __global__ __launch_bounds__(256, sizeof(PrepSmem<T, DK, DV>) <= 80 * 1024 ? 2 :
     const int g16 = lane >> 4, c16 = lane & 15;
     int64_t j;
     int seq, h;
-    if (!unit_of_block(a.n_seqs, a.n_heads, a.max_chunks, &seq, &h, &j)) return;
+    if (!unit_of_block(a.n_seqs, a.n_heads, a.max_chunks, a.chunk_major != 0, &seq, &h, &j)) return;
     const int H = a.n_heads;
     const int64_t cu0 = a.cu[seq];
     const int len = a.cu[seq + 1] - a.cu[seq];

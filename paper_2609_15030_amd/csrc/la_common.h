@@ -186,32 +186,57 @@ __device__ __host__ inline int64_t total_slots(int64_t total_tokens, int64_t n_s
 }
 
 // ---------------------------------------------------------------------------
-// XCD-aware block mapping.  Workgroups are dealt to the 8 XCDs round-robin by
-// linear id; each XCD has its own L2.  (sequence, head) pair p is pinned to
-// XCD p % 8 in every kernel of the prefill, so the chunk intermediates one
-// kernel writes for that pair are read back from the same L2 by the next.
-// Per-chunk kernels use a 1-D grid of 8 * max_chunks * ceil(pairs / 8)
-// blocks: block id = 8 * (chunk + max_chunks * (p / 8)) + p % 8.
+// XCD-aware block mapping of the per-chunk kernels.  Workgroups are dealt to
+// the 8 XCDs round-robin by linear id; each XCD has its own L2.  Two maps:
+//   pair-major: (sequence, head) pair p goes to XCD p % 8, as in the scan
+//     kernels, so a chain's chunks are prepared where it is scanned;
+//     block id = 8 * (chunk + max_chunks * (p / 8)) + p % 8;
+//   chunk-major: the units of chunk c of a sequence, for every head, go to
+//     XCD c % 8, so the chunk's gates and betas (stored [token, head]: a
+//     cache line holds a few tokens of every head) are fetched once into one
+//     L2 rather than once per head into several; block id =
+//     8 * ((seq * CG + c / 8) * H + head) + c % 8, CG = ceil(max_chunks / 8).
+// The host takes chunk-major for launches of many units, where the gathers'
+// traffic counts, and pair-major otherwise.
 // ---------------------------------------------------------------------------
-__device__ inline bool unit_of_block(int n_seqs, int n_heads, int max_chunks, int *seq, int *head,
-                                     int64_t *chunk) {
+constexpr int64_t kChunkMajorUnits = 2048;
+
+__host__ inline bool chunk_major_map(int n_seqs, int n_heads, int64_t max_chunks) {
+    return (int64_t)n_seqs * n_heads * max_chunks > kChunkMajorUnits;
+}
+
+__device__ inline bool unit_of_block(int n_seqs, int n_heads, int max_chunks, bool chunk_major, int *seq,
+                                     int *head, int64_t *chunk) {
     // 32-bit arithmetic: a 64-bit division costs hundreds of cycles at the
-    // start of every workgroup (grids and n_seqs * n_heads stay below 2^32)
+    // start of every workgroup (grids stay below 2^32)
     const uint32_t b = blockIdx.x;
-    const uint32_t r = b >> 3;
-    const uint32_t q = r / (uint32_t)max_chunks;
-    const uint32_t pair = (b & 7) + 8 * q;
-    if (pair >= (uint32_t)n_seqs * (uint32_t)n_heads) return false;
-    *chunk = (int64_t)(r - q * (uint32_t)max_chunks);
-    const uint32_t sq = pair / (uint32_t)n_heads;
+    const uint32_t x = b & 7, m = b >> 3;
+    const uint32_t H = (uint32_t)n_heads;
+    uint32_t sq, hd, c;
+    if (chunk_major) {
+        const uint32_t CG = ((uint32_t)max_chunks + 7) / 8;
+        const uint32_t t = m / H;
+        hd = m - t * H;
+        sq = t / CG;
+        c = 8 * (t - sq * CG) + x;
+        if (sq >= (uint32_t)n_seqs || c >= (uint32_t)max_chunks) return false;
+    } else {
+        const uint32_t q = m / (uint32_t)max_chunks;
+        const uint32_t pair = x + 8 * q;
+        if (pair >= (uint32_t)n_seqs * H) return false;
+        c = m - q * (uint32_t)max_chunks;
+        sq = pair / H;
+        hd = pair - sq * H;
+    }
     *seq = (int)sq;
-    *head = (int)(pair - sq * (uint32_t)n_heads);
+    *head = (int)hd;
+    *chunk = (int64_t)c;
     return true;
 }
 
 __host__ inline int64_t chunk_grid_blocks(int n_seqs, int n_heads, int64_t max_chunks) {
-    const int64_t pairs = (int64_t)n_seqs * n_heads;
-    return 8 * max_chunks * ((pairs + 7) / 8);
+    if (chunk_major_map(n_seqs, n_heads, max_chunks)) return 8 * ((max_chunks + 7) / 8) * (int64_t)n_seqs * n_heads;
+    return 8 * max_chunks * (((int64_t)n_seqs * n_heads + 7) / 8);
 }
 
 // ---------------------------------------------------------------------------

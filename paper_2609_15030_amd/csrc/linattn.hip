@@ -269,7 +269,8 @@ la_status launch_out(const PrefillCall &c, const la::Workspace &ws, int64_t max_
     if (trace) (void)hipEventRecord((hipEvent_t)g_trace[2], c.stream);
     if (max_chunks > 0 && (c.stages & LA_STAGE_OUTPUT)) {
         la::OutArgs oa{c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
-                       (int32_t)max_chunks, s->scale, ws};
+                       (int32_t)max_chunks, s->scale, ws,
+                       la::chunk_major_map(s->n_seqs, s->n_heads, max_chunks) ? 1 : 0};
         const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
         hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(4 * DV), 0, c.stream, oa);
         if (la_status e = hip_check("output launch")) return e;
@@ -361,7 +362,8 @@ la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chun
 
     if (max_chunks > 0 && (c.stages & LA_STAGE_PREPARE)) {
         la::PrepArgs pa{c.q, c.k, c.v, c.g, c.beta, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
-                        s->variant, (int32_t)max_chunks, ws};
+                        s->variant, (int32_t)max_chunks, ws,
+                        la::chunk_major_map(s->n_seqs, s->n_heads, max_chunks) ? 1 : 0};
         const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
         hipLaunchKernelGGL((la::gdr_prep_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(256), 0, c.stream, pa);
         if (la_status e = hip_check("chunk preparation launch")) return e;
