@@ -312,10 +312,11 @@ def bench_hybrid(la, torch, stream_ptr, events, n_tokens, interval, n_heads, pag
         for _ in range(3):
             la.la_hybrid_restore(kv, bdev, [B], stp, sid, states, n_heads)
         torch.cuda.synchronize()
-        # one event pair per launch: the entry point's host-side checks of the
-        # pools take about as long as a device-pool restore, so an interval
-        # over back-to-back launches would hold host time whenever the GPU
-        # waits for the next launch
+        # One event pair per launch, all queued behind a GPU spin: the entry
+        # point's host-side checks of the pools (pointer-attribute queries)
+        # take from a few to ~60 us, longer than a device-pool restore, so an
+        # idle GPU would wait for each launch inside its own interval.
+        torch.cuda._sleep(20_000_000)
         ev = HipEvents(2 * reps)
         for r in range(reps):
             ev.record(2 * r, stream_ptr)
