@@ -157,40 +157,44 @@ la_status la_prefill_resume(const la_shape *shape,
                             void *workspace, size_t ws_bytes, void *stream);
 
 /*
- * la_prefill_stages - run a subset of one prefill call's stages, so that a
- * caller can overlap them with other work.  The preparation of a resume
- * depends only on the suffix tokens (section 2.2: the scheduled tokens), so
- * it can run while the state for prefix [0, B) is still being saved or
- * restored (section 3.1), and one call's output can run beside the next
- * call's scan.  `stages` is a mask of
- *   LA_STAGE_PREPARE (1): chunk-local gate sums and the intra-chunk operands
- *                         (from q, k, v, g, beta) into the workspace;
- *   LA_STAGE_SCAN    (2): the inter-chunk recurrence from state_in (or zero):
- *                         checkpoints and the final state, plus the per-chunk
- *                         states the output needs, into the workspace;
- *   LA_STAGE_OUTPUT  (4): o from the workspace.
- * A call that runs SCAN and OUTPUT together computes o inside the scan
- * kernel; split calls compute the same o bit for bit.
- * Arguments as la_prefill_resume; start_pos_dev/host NULL make it a cold
- * call, and then state_in must be NULL.  Every call validates all arguments.
- * The stages of one call must run in that order on one workspace with the
- * same arguments; ordering them across streams (events) is the caller's.
- * la_prefill and la_prefill_resume run all three stages.
+ * la_checkpoint_rows - the checkpoint row numbering of one call, so that
+ * callers need not re-derive it.  Sequence i (suffix length
+ * cu[i+1] - cu[i], starting at absolute position B_i = start_pos_host[i], or
+ * 0 when start_pos_host is NULL) owns the checkpoints at the absolute
+ * multiples P of C with B_i < P <= B_i + len_i (section 2.2: the state for
+ * prefix [0, P)), numbered consecutively from offsets_out[i]; the sequences'
+ * blocks follow one another in order.  Writes offsets_out[n_seqs] and the
+ * total row count.  Host only; errors: LA_ERR_INVALID_ARG for a decreasing
+ * cu_seqlens, C < 1, a negative start or more than 2^31 rows.
  */
-#define LA_STAGE_PREPARE 1u
-#define LA_STAGE_SCAN 2u
-#define LA_STAGE_OUTPUT 4u
-#define LA_STAGE_ALL 7u
-la_status la_prefill_stages(const la_shape *shape, uint32_t stages,
-                            const void *q, const void *k, const void *v,
-                            const float *g, const float *beta,
-                            const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
-                            const int64_t *start_pos_dev, const int64_t *start_pos_host,
-                            const float *state_in,
-                            void *o, float *final_state,
-                            float *ckpt_out, const int32_t *ckpt_offsets_dev,
-                            const int32_t *ckpt_offsets_host,
-                            void *workspace, size_t ws_bytes, void *stream);
+la_status la_checkpoint_rows(int32_t n_seqs, const int32_t *cu_seqlens_host, const int64_t *start_pos_host,
+                             int64_t interval, int32_t *offsets_out, int64_t *total_rows_out);
+
+/*
+ * la_prefill_form - which kernels a prefill call of this shape runs.  The
+ * form depends on the shape alone (never on the lengths), so a resume always
+ * runs the arithmetic of the call that wrote its checkpoint:
+ *   LA_FORM_FUSED_SCAN        bf16, checkpoint intervals below 8 chunks:
+ *                             the chunk preparation, then one fused scan
+ *                             (recurrence, output, checkpoints) per
+ *                             (sequence, head);
+ *   LA_FORM_FUSED_TWO_LEVEL   bf16, intervals of 8 chunks or more (C > 448):
+ *                             the preparation, segment maps, the sequential
+ *                             combine over segments and the fused replay;
+ *   LA_FORM_TILE_SCAN_OUT     fp32, dk = 64: per-chunk operands, then one
+ *                             scan wave and one output wave per 16 columns;
+ *   LA_FORM_SPLIT_DK_SCAN     fp32, dk = 128: per-chunk operands, a scan
+ *                             whose waves split dk, and the output kernel.
+ * LA_FORM_NONE for an invalid or unsupported shape.  Host only.
+ */
+typedef enum la_form {
+    LA_FORM_NONE = 0,
+    LA_FORM_FUSED_SCAN = 1,
+    LA_FORM_FUSED_TWO_LEVEL = 2,
+    LA_FORM_TILE_SCAN_OUT = 3,
+    LA_FORM_SPLIT_DK_SCAN = 4
+} la_form;
+la_form la_prefill_form(const la_shape *shape);
 
 /*
  * la_prefill_paged - a prefill (cold or resumed) whose checkpoints go

@@ -64,14 +64,11 @@ def to_device(x: Inputs, device="cuda") -> DeviceInputs:
                         dev(x.beta, torch.float32), dev(cu, torch.int32), cu, io)
 
 
-def checkpoint_rows(lengths: Sequence[int], starts: Sequence[int], interval: int):
-    """Row offsets for the checkpoints of each sequence (absolute multiples of
-    C in (B_i, B_i + len_i]) packed back to back; returns (offsets, total)."""
-    offs, row = [], 0
-    for n, b in zip(lengths, starts):
-        offs.append(row)
-        row += (b + n) // interval - b // interval
-    return np.asarray(offs, np.int32), row
+def checkpoint_rows(lengths: Sequence[int], starts: Optional[Sequence[int]], interval: int):
+    """Row offsets for the checkpoints of each sequence and the total, as the
+    library numbers them (la_checkpoint_rows)."""
+    cu = np.concatenate([[0], np.cumsum(np.asarray(lengths, np.int64))]).astype(np.int32)
+    return la.la_checkpoint_rows(cu, None if starts is None else np.asarray(starts, np.int64), interval)
 
 
 @dataclasses.dataclass
@@ -95,8 +92,7 @@ class Prefill:
         dev = x.q.device
         lens = np.diff(x.cu_host).tolist()
         self.starts = None if starts is None else np.asarray(starts, np.int64)
-        b = [0] * len(lens) if starts is None else list(starts)
-        self.ckpt_offsets, self.n_ckpt_rows = checkpoint_rows(lens, b, interval)
+        self.ckpt_offsets, self.n_ckpt_rows = checkpoint_rows(lens, starts, interval)
         self.ckpt_off_dev = torch.from_numpy(self.ckpt_offsets).to(dev)
         self.start_dev = None if starts is None else torch.from_numpy(self.starts).to(dev)
         self.o = torch.empty((x.total_tokens, x.n_heads, x.dv), dtype=x.q.dtype, device=dev)
@@ -109,19 +105,10 @@ class Prefill:
         assert nbytes > 0
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
 
-    def run(self, state_in: Optional[torch.Tensor] = None, stream=None, stages: int = la.LA_STAGE_ALL) -> PrefillResult:
-        """All stages (la_prefill / la_prefill_resume), or the subset ``stages``
-        (la_prefill_stages) for callers that overlap stages with other work."""
+    def run(self, state_in: Optional[torch.Tensor] = None, stream=None) -> PrefillResult:
+        """la_prefill (cold) or la_prefill_resume (with start positions)."""
         x = self.x
         ck = self.ckpt
-        if stages != la.LA_STAGE_ALL:
-            if self.starts is not None:
-                assert state_in is not None
-            la.la_prefill_stages(self.shape, stages, x.q, x.k, x.v, x.g, x.beta, x.cu_dev, x.cu_host,
-                                 self.start_dev, self.starts, state_in if self.starts is not None else None,
-                                 self.o, self.final, ck, self.ckpt_off_dev if ck is not None else None,
-                                 self.ckpt_offsets if ck is not None else None, self.workspace, stream)
-            return PrefillResult(self.o, self.final, ck, self.ckpt_offsets, self.n_ckpt_rows)
         if self.starts is None:
             la.la_prefill(self.shape, x.q, x.k, x.v, x.g, x.beta, x.cu_dev, x.cu_host, self.o,
                           self.final, ck, self.ckpt_off_dev if ck is not None else None,

@@ -73,8 +73,9 @@ struct ScanArgs {
     Workspace ws;
     int32_t seg_m, max_seg;       // two-level scan only
     SegWorkspace seg;
-    void *o;                      // scan with output wave only: output [T, H, dv] (io type)
+    void *o;                      // scans with output: output [T, H, dv] (io type)
     float scale;
+    const void *q, *k, *v;        // fused scan: the inputs [T, H, dk | dv] (bf16)
     PageIO pg;
     ChainOrder order;
 };

@@ -14,9 +14,8 @@
 #include "la_common.h"
 #include "gdr_prep.h"
 #include "gdr_scan.h"
-#include "gdr_group.h"
-#include "gdr_scan_pair.h"
 #include "gdr_out.h"
+#include "gdr_xscan.h"
 #include "gdr_decode.h"
 #include "paged.h"
 #include "hybrid.h"
@@ -47,123 +46,7 @@ constexpr size_t kRegionAlign = 256;
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Scan kernel form: 1 = one wave per 16-column tile, 4 = DK/32 waves sharing
-// the tile's state rows.  The single-wave form has the shorter chain; with
-// fp32 operands at dk = 128 it does not fit the register file, so that case
-// splits dk.  LA_SCAN_WAVES=1|4 overrides the choice (for tuning).
-int scan_variant(bool f32, int dk) {
-    static const int forced = [] {
-        const char *e = getenv("LA_SCAN_WAVES");
-        return e ? atoi(e) : 0;
-    }();
-    if (forced == 1 || forced == 4) return forced;
-    return (f32 && dk == 128) ? 4 : 1;
-}
-
 size_t io_size(int32_t dtype) { return dtype == LA_BF16 ? 2 : 4; }
-
-// Whether a call that runs the scan and output stages together uses the
-// single-wave scan's output wave (one kernel) instead of the split output
-// kernel or the workgroup scan; all give identical bits.  The
-// scan-with-output workgroup holds two waves with a large register file
-// each, so few of them fit on a CU, and each is one sequential chain: a
-// launch that needs more rounds of residency than it has chains per round
-// runs its later chains after the first ones end.  fp32 operands use it
-// only while every workgroup is resident at once; bf16 up to two rounds
-// (on a 16-sequence, 8-head batch of 1,024 tiles with 512 resident it beat
-// both the split kernels, whose state and U make a round trip through HBM,
-// and the workgroup scan, bound by its CU's LDS bandwidth).
-// LA_SCAN_OUTPUT=0 selects the split kernels (for measurement).
-bool output_waves_on() {
-    static const bool on = [] {
-        const char *e = getenv("LA_SCAN_OUTPUT");
-        return !(e && atoi(e) == 0);
-    }();
-    return on;
-}
-
-template <typename T, int DK, int DV>
-bool scan_with_output(int64_t blocks) {
-    if (!output_waves_on()) return false;
-    static int64_t capacity[64] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
-        (void)hipGetLastError();
-        return false;
-    }
-    if (capacity[dev] == 0) {
-        int per_cu = 0, cus = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, la::gdr_scan1o_kernel<T, DK, DV>, 128, 0) !=
-                hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
-            (void)hipGetLastError();
-            return false;
-        }
-        capacity[dev] = (int64_t)per_cu * cus;
-    }
-    const int64_t rounds = sizeof(T) == 2 ? 2 : 1;
-    return blocks <= rounds * capacity[dev];
-}
-
-// Workgroups of `kernel` (launched with `threads` lanes) resident on the
-// current device at once; cached per device and caller slot.  0 when the
-// runtime cannot say.
-template <typename K>
-int64_t resident_capacity(K kernel, int threads, int slot) {
-    static int64_t cache[4][64] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64 || slot < 0 || slot >= 4) {
-        (void)hipGetLastError();
-        return 0;
-    }
-    if (cache[slot][dev] == 0) {
-        int per_cu = 0, cus = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
-            (void)hipGetLastError();
-            return 0;
-        }
-        cache[slot][dev] = (int64_t)per_cu * cus;
-    }
-    return cache[slot][dev];
-}
-
-// Whether a bf16 call with the scan and output stages runs the scan with
-// output wave over pairs of column tiles (gdr_scan2o_kernel) instead of one
-// tile per workgroup: when the one-tile workgroups do not all fit at once
-// but the pair workgroups fit in two rounds.  Several scan workgroups then
-// share each CU, whose load path bounds their chunk steps, and a pair moves
-// half the operand bytes per tile (16-sequence, 8-head varlen batch:
-// 1,024 one-tile or 512 pair workgroups).  LA_SCAN_PAIR=1|0 forces the
-// choice (for measurement).
-template <typename T, int DK, int DV>
-bool scan_by_pairs(int64_t blocks1, int64_t blocks2) {
-    static const int forced = [] {
-        const char *e = getenv("LA_SCAN_PAIR");
-        return e ? atoi(e) : -1;
-    }();
-    if (forced == 0 || forced == 1) return forced == 1;
-    if (!output_waves_on()) return false;
-    const int64_t cap1 = resident_capacity(la::gdr_scan1o_kernel<T, DK, DV>, 128, 0);
-    const int64_t cap2 = resident_capacity(la::gdr_scan2o_kernel<T, DK, DV>, 128, 1);
-    return cap1 > 0 && cap2 > 0 && blocks1 > cap1 && blocks2 <= 2 * cap2;
-}
-
-// Whether a single-level bf16 scan runs as one workgroup per (sequence,
-// head) chain (the chunk operands shared through LDS, output waves beside
-// the scan waves) instead of one wave per 16-column tile.  By default the
-// workgroup form serves the calls that include the output stage and have
-// more tiles than the per-tile scan with output wave takes (see
-// scan_with_output); the split kernels' output would make a round trip
-// through HBM.  LA_SCAN_GROUP=1|0 forces the choice (for measurement).
-bool scan_by_group(bool tile_scan_with_output, bool output_stage) {
-    static const int forced = [] {
-        const char *e = getenv("LA_SCAN_GROUP");
-        return e ? atoi(e) : -1;
-    }();
-    if (forced == 0 || forced == 1) return forced == 1;
-    return output_stage && !tile_scan_with_output && output_waves_on();
-}
 
 // Chunks per segment of the two-level scan (1 = single-level).  A segment
 // must divide a checkpoint interval's chunks, so every checkpoint position is
@@ -173,19 +56,26 @@ bool scan_by_group(bool tile_scan_with_output, bool output_stage) {
 // largest such divisor up to 16 balances the two parallel levels against the
 // sequential combine.  Intervals of fewer than 8 chunks keep the
 // single-level scan: there a segment's map costs more than the chunks it
-// replaces.  bf16 operands only.  LA_SCAN_LEVELS=1|2 forces one form (for
-// tuning).
+// replaces.  bf16 operands only.
 int seg_chunks(const la_shape *s) {
-    static const int forced = [] {
-        const char *e = getenv("LA_SCAN_LEVELS");
-        return e ? atoi(e) : 0;
-    }();
-    if (forced == 1 || s->io_dtype != LA_BF16) return 1;
+    if (s->io_dtype != LA_BF16) return 1;
     const int cps = la::chunks_per_interval(s->ckpt_interval);
-    if (forced != 2 && cps < 8) return 1;
+    if (cps < 8) return 1;
     for (int m = std::min(cps, 16); m >= 2; --m)
         if (cps % m == 0) return m;
     return 1;
+}
+
+// The kernels a prefill call runs, a function of its shape alone (so a
+// resume and the run that wrote its checkpoint always take the same form):
+//   bf16: the preparation, then the fused scan (single-level), or the
+//         segment maps, the combine and the fused replay (two-level);
+//   fp32: the per-chunk preparation, then the one-tile scan with its output
+//         wave (dk = 64), or the dk-split scan and the output kernel (dk = 128,
+//         whose one-tile state does not fit the register file).
+la_form prefill_form(const la_shape *s) {
+    if (s->io_dtype == LA_BF16) return seg_chunks(s) > 1 ? LA_FORM_FUSED_TWO_LEVEL : LA_FORM_FUSED_SCAN;
+    return s->dk == 128 ? LA_FORM_SPLIT_DK_SCAN : LA_FORM_TILE_SCAN_OUT;
 }
 
 bool shape_supported(const la_shape *s) {
@@ -208,9 +98,16 @@ la_status check_shape(const la_shape *s) {
     return LA_OK;
 }
 
+// Workspace regions (byte offsets; 0 = absent).  Per chunk slot and head:
+//   bf16: X fragments (6 KB) and the gate block (1 KB);
+//   fp32: -W, K~^T, U~, G, P and Q in operand order, plus the state entering
+//         each chunk and U for the output kernel of the dk-split scan.
+// The two-level scan adds, per segment slot and head, Phi' (io type), R, D
+// and the state entering the segment.
 struct WsPlan {
-    size_t w, kt, ut, g, sc, u, pm, qf;      // byte offsets of each region
-    size_t phi, segr, segd, segst;           // two-level scan regions (seg_m >= 2)
+    size_t xf, gb;                           // bf16 forms
+    size_t w, kt, ut, g, sc, u, pm, qf;      // fp32 forms
+    size_t phi, segr, segd, segst;           // two-level scan (seg_m >= 2)
     int seg_m;
     size_t total;
 };
@@ -220,19 +117,26 @@ WsPlan plan_workspace(const la_shape *s, int64_t total_tokens) {
     const int64_t slots = la::total_slots(total_tokens, s->n_seqs, s->ckpt_interval, cps);
     const size_t sh = (size_t)slots * s->n_heads;
     const size_t io = io_size(s->io_dtype);
-    WsPlan p;
-    size_t off = 0;
+    const la_form form = prefill_form(s);
+    WsPlan p{};
+    size_t off = kRegionAlign;   // offset 0 marks an absent region
     auto take = [&](size_t bytes) { const size_t at = off; off = round_up(off + bytes, kRegionAlign); return at; };
-    p.w = take(sh * la::kChunk * s->dk * io);
-    p.kt = take(sh * s->dk * la::kChunk * io);
-    p.ut = take(sh * la::kChunk * s->dv * io);
-    p.g = take(sh * la::kChunk * sizeof(float));
-    p.sc = take(sh * (size_t)s->dk * s->dv * io);
-    p.u = take(sh * la::kChunk * s->dv * io);
-    p.pm = take(sh * la::kChunk * la::kChunk * io);
-    p.qf = take(sh * la::kChunk * s->dk * io);
+    if (s->io_dtype == LA_BF16) {
+        p.xf = take(sh * la::kXFrags * 64 * 16);
+        p.gb = take(sh * la::kGateBlock * sizeof(float));
+    } else {
+        p.w = take(sh * la::kChunk * s->dk * io);
+        p.kt = take(sh * s->dk * la::kChunk * io);
+        p.ut = take(sh * la::kChunk * s->dv * io);
+        p.g = take(sh * la::kChunk * sizeof(float));
+        p.pm = take(sh * la::kChunk * la::kChunk * io);
+        p.qf = take(sh * la::kChunk * s->dk * io);
+        if (form == LA_FORM_SPLIT_DK_SCAN) {
+            p.sc = take(sh * (size_t)s->dk * s->dv * io);
+            p.u = take(sh * la::kChunk * s->dv * io);
+        }
+    }
     p.seg_m = seg_chunks(s);
-    p.phi = p.segr = p.segd = p.segst = 0;
     if (p.seg_m > 1) {
         const int64_t seg_slots = la::total_slots(total_tokens, s->n_seqs, s->ckpt_interval * (int64_t)p.seg_m, cps);
         const size_t ssh = (size_t)seg_slots * s->n_heads;
@@ -241,7 +145,7 @@ WsPlan plan_workspace(const la_shape *s, int64_t total_tokens) {
         p.segd = take(ssh * sizeof(float));
         p.segst = take(ssh * s->dk * s->dv * sizeof(float));
     }
-    p.total = std::max<size_t>(off, kRegionAlign);
+    p.total = off;
     return p;
 }
 
@@ -258,72 +162,19 @@ struct PrefillCall {
     void *workspace;
     size_t ws_bytes;
     hipStream_t stream;
-    uint32_t stages = LA_STAGE_ALL;
     const la_pages *pages = nullptr;         // paged checkpoints / starting states
 };
 
-template <typename T, int DK, int DV>
-la_status launch_out(const PrefillCall &c, const la::Workspace &ws, int64_t max_chunks, bool trace) {
-    const la_shape *s = c.shape;
-    const int cps = la::chunks_per_interval(s->ckpt_interval);
-    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[2], c.stream);
-    if (max_chunks > 0 && (c.stages & LA_STAGE_OUTPUT)) {
-        la::OutArgs oa{c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
-                       (int32_t)max_chunks, s->scale, ws,
-                       la::chunk_major_map(s->n_seqs, s->n_heads, max_chunks) ? 1 : 0};
-        const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
-        hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(4 * DV), 0, c.stream, oa);
-        if (la_status e = hip_check("output launch")) return e;
-    }
-    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[3], c.stream);
-    return LA_OK;
-}
-
-// Two-level scan: segment maps (all segments at once), the sequential
-// combine over segments, then every segment replayed from its entering
-// state; then the output kernel.
-template <typename T, int DK, int DV>
-la_status launch_two_level(const PrefillCall &c, const WsPlan &p, la::ScanArgs sa, int64_t max_chunks,
-                           bool trace) {
-    const la_shape *s = c.shape;
-    char *base = (char *)c.workspace;
-    sa.seg_m = p.seg_m;
-    sa.max_seg = (int32_t)((max_chunks + p.seg_m - 1) / p.seg_m);
-    sa.seg.phi = base + p.phi;
-    sa.seg.r = (float *)(base + p.segr);
-    sa.seg.d = (float *)(base + p.segd);
-    sa.seg.state = (float *)(base + p.segst);
-    constexpr int NT = DV / 16;
-    const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
-    const int64_t units = pairs * sa.max_seg;
-    if (units > 0) {
-        hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupTrans>), dim3((unsigned)units),
-                           dim3(64 * la::group_scan_waves<DK, DV, la::kGroupTrans>()), 0, c.stream, sa);
-        if (la_status e = hip_check("segment map launch")) return e;
-    }
-    hipLaunchKernelGGL((la::gdr_seg_combine_kernel<T, DK, DV>), dim3((unsigned)(8 * NT * ((pairs + 7) / 8))),
-                       dim3(64), 0, c.stream, sa);
-    if (la_status e = hip_check("segment combine launch")) return e;
-    // the replay's output waves produce the output when the call includes
-    // the output stage; otherwise the split output kernel reads the states
-    // and U the replay leaves in the workspace
-    const bool out_stage = (c.stages & LA_STAGE_OUTPUT) != 0 && output_waves_on();
-    if (units > 0) {
-        if (out_stage)
-            hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupReplay, true>), dim3((unsigned)units),
-                               dim3(128 * la::kGroupWaves), 0, c.stream, sa);
-        else
-            hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupReplay>), dim3((unsigned)units),
-                               dim3(64 * la::kGroupWaves), 0, c.stream, sa);
-        if (la_status e = hip_check("segment replay launch")) return e;
-    }
-    return launch_out<T, DK, DV>(c, sa.ws, out_stage ? 0 : max_chunks, trace);
+// Profiling hook (la_trace_set_events): events recorded on the launch stream
+// at the start, after the preparation, after the scan and at the end.
+void trace_mark(int i, hipStream_t stream) {
+    if (g_trace_n >= 4) (void)hipEventRecord((hipEvent_t)g_trace[i], stream);
 }
 
 // Ranks the (sequence, head) chains for dispatch, longest first (equal
-// lengths keep sequence order), so the workgroups each CU receives mix long
-// and short chains.  Batches of more than kChainOrderMax chains, or of one
-// sequence, keep the natural order.
+// lengths keep sequence order), so the long chains start first.  Batches of
+// more than kChainOrderMax chains, or of one sequence, keep the natural
+// order.
 void order_chains(const PrefillCall &c, la::ChainOrder &order) {
     const la_shape *s = c.shape;
     const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
@@ -341,106 +192,159 @@ void order_chains(const PrefillCall &c, la::ChainOrder &order) {
     order.n = (int32_t)pairs;
 }
 
-template <typename T, int DK, int DV>
-la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) {
+la::ScanArgs scan_args(const PrefillCall &c, const la::Workspace &ws) {
+    const la_shape *s = c.shape;
+    la::ScanArgs sa{};
+    sa.cu = c.cu_dev;
+    sa.state_in = c.state_in;
+    sa.final_state = c.final_state;
+    sa.ckpt = c.ckpt_out;
+    sa.ckpt_off = c.ckpt_off_dev;
+    sa.n_seqs = s->n_seqs;
+    sa.n_heads = s->n_heads;
+    sa.C = s->ckpt_interval;
+    sa.cps = la::chunks_per_interval(s->ckpt_interval);
+    sa.ws = ws;
+    sa.seg_m = 1;
+    sa.max_seg = 1;
+    sa.q = c.q;
+    sa.k = c.k;
+    sa.v = c.v;
+    sa.o = c.o;
+    sa.scale = s->scale;
+    if (c.pages) {
+        sa.pg.pool = c.pages->pool;
+        sa.pg.ckpt_ids = c.pages->ckpt_page_ids;
+        sa.pg.state_ids = c.pages->state_page_ids;
+        sa.pg.err = c.pages->err_count;
+        sa.pg.n_pages = (int32_t)c.pages->n_pages;
+    }
+    order_chains(c, sa.order);
+    return sa;
+}
+
+// bf16: preparation, then the fused scan, or the two-level scan (segment
+// maps, combine, fused replay).
+template <int DK, int DV>
+la_status launch_fused(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) {
     const la_shape *s = c.shape;
     const int cps = la::chunks_per_interval(s->ckpt_interval);
     char *base = (char *)c.workspace;
-    la::Workspace ws;
+    la::Workspace ws{};
+    ws.xf = base + p.xf;
+    ws.gb = (float *)(base + p.gb);
+    trace_mark(0, c.stream);
+    (void)hipGetLastError();
+    if (max_chunks > 0) {
+        la::XPrepArgs pa{c.k, c.g, c.beta, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps, s->variant,
+                         (int32_t)max_chunks, ws.xf, ws.gb,
+                         la::chunk_major_map(s->n_seqs, s->n_heads, max_chunks) ? 1 : 0};
+        const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
+        hipLaunchKernelGGL((la::gdr_xprep_kernel<DK>), dim3((unsigned)blocks), dim3(256), 0, c.stream, pa);
+        if (la_status e = hip_check("chunk preparation launch")) return e;
+    }
+    trace_mark(1, c.stream);
+    la::ScanArgs sa = scan_args(c, ws);
+    constexpr int CW = la::xscan_cols<DK, DV>();
+    constexpr int NP = DV / CW, NPM = (DK + DV) / CW;
+    const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
+    if (p.seg_m > 1) {
+        sa.seg_m = p.seg_m;
+        sa.max_seg = (int32_t)((max_chunks + p.seg_m - 1) / p.seg_m);
+        sa.seg.phi = base + p.phi;
+        sa.seg.r = (float *)(base + p.segr);
+        sa.seg.d = (float *)(base + p.segd);
+        sa.seg.state = (float *)(base + p.segst);
+        const int64_t units = pairs * sa.max_seg;
+        if (units > 0) {
+            hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, la::kXMap>), dim3((unsigned)(8 * NPM * ((units + 7) / 8))),
+                               dim3(2 * CW), 0, c.stream, sa);
+            if (la_status e = hip_check("segment map launch")) return e;
+        }
+        hipLaunchKernelGGL((la::gdr_seg_combine_kernel<__bf16, DK, DV>), dim3((unsigned)(8 * (DV / 16) * ((pairs + 7) / 8))),
+                           dim3(64), 0, c.stream, sa);
+        if (la_status e = hip_check("segment combine launch")) return e;
+        if (units > 0) {
+            hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, la::kXReplay>), dim3((unsigned)(8 * NP * ((units + 7) / 8))),
+                               dim3(2 * CW), 0, c.stream, sa);
+            if (la_status e = hip_check("segment replay launch")) return e;
+        }
+    } else {
+        hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, la::kXScan>), dim3((unsigned)(8 * NP * ((pairs + 7) / 8))),
+                           dim3(2 * CW), 0, c.stream, sa);
+        if (la_status e = hip_check("fused scan launch")) return e;
+    }
+    trace_mark(2, c.stream);
+    trace_mark(3, c.stream);
+    return LA_OK;
+}
+
+// fp32: per-chunk preparation, then the one-tile scan with its output wave
+// (dk = 64), or the dk-split scan and the split output kernel (dk = 128).
+template <int DK, int DV>
+la_status launch_f32(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) {
+    typedef float T;
+    const la_shape *s = c.shape;
+    const int cps = la::chunks_per_interval(s->ckpt_interval);
+    char *base = (char *)c.workspace;
+    la::Workspace ws{};
     ws.w = base + p.w;
     ws.kt = base + p.kt;
     ws.ut = base + p.ut;
     ws.g = (float *)(base + p.g);
-    ws.sc = base + p.sc;
-    ws.u = base + p.u;
+    ws.sc = p.sc ? base + p.sc : nullptr;
+    ws.u = p.u ? base + p.u : nullptr;
     ws.p = base + p.pm;
     ws.qf = base + p.qf;
-
-    const bool trace = g_trace_n >= 4;
-    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[0], c.stream);
+    const int32_t chunk_major = la::chunk_major_map(s->n_seqs, s->n_heads, max_chunks) ? 1 : 0;
+    trace_mark(0, c.stream);
     (void)hipGetLastError();
-
-    if (max_chunks > 0 && (c.stages & LA_STAGE_PREPARE)) {
+    if (max_chunks > 0) {
         la::PrepArgs pa{c.q, c.k, c.v, c.g, c.beta, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps,
-                        s->variant, (int32_t)max_chunks, ws,
-                        la::chunk_major_map(s->n_seqs, s->n_heads, max_chunks) ? 1 : 0};
+                        s->variant, (int32_t)max_chunks, ws, chunk_major};
         const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
         hipLaunchKernelGGL((la::gdr_prep_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(256), 0, c.stream, pa);
         if (la_status e = hip_check("chunk preparation launch")) return e;
     }
-    if (trace) (void)hipEventRecord((hipEvent_t)g_trace[1], c.stream);
-    if (c.stages & LA_STAGE_SCAN) {
-        la::ScanArgs sa{c.cu_dev, c.state_in, c.final_state, c.ckpt_out, c.ckpt_off_dev,
-                        s->n_seqs, s->n_heads, s->ckpt_interval, cps, ws, 1, 0, {},
-                        c.o, s->scale, {}};
-        if (c.pages) {
-            sa.pg.pool = c.pages->pool;
-            sa.pg.ckpt_ids = c.pages->ckpt_page_ids;
-            sa.pg.state_ids = c.pages->state_page_ids;
-            sa.pg.err = c.pages->err_count;
-            sa.pg.n_pages = (int32_t)c.pages->n_pages;
-        }
-        constexpr int NT = DV / 16;
-        const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
-        const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
-        order_chains(c, sa.order);
-        if constexpr (sizeof(T) == 2) {
-            if (p.seg_m > 1) return launch_two_level<T, DK, DV>(c, p, sa, max_chunks, trace);
-        }
-        const bool out_stage = (c.stages & LA_STAGE_OUTPUT) != 0;
-        if constexpr (sizeof(T) == 2) {
-            const int64_t blocks2 = 8 * (NT / la::kPairTiles) * ((pairs + 7) / 8);
-            if (out_stage && scan_variant(false, DK) == 1 && scan_by_pairs<T, DK, DV>(blocks, blocks2)) {
-                hipLaunchKernelGGL((la::gdr_scan2o_kernel<T, DK, DV>), dim3((unsigned)blocks2), dim3(128), 0,
-                                   c.stream, sa);
-                if (la_status e = hip_check("inter-chunk scan launch")) return e;
-                return launch_out<T, DK, DV>(c, ws, 0, trace);
-            }
-        }
-        const bool with_out = scan_variant(sizeof(T) == 4, DK) == 1 && out_stage && scan_with_output<T, DK, DV>(blocks);
-        if constexpr (sizeof(T) == 2) {
-            // the workgroup scan stands in for the single-wave form only (the
-            // dk-split scan sums its partial products in another order)
-            if (scan_variant(false, DK) == 1 && scan_by_group(with_out, out_stage)) {
-                // one workgroup per (sequence, head) chain: 4 scan waves, and
-                // 4 output waves when the call includes the output stage
-                sa.seg_m = 1;
-                sa.max_seg = 1;
-                if (out_stage)
-                    hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupScan, true>), dim3((unsigned)pairs),
-                                       dim3(128 * la::kGroupWaves), 0, c.stream, sa);
-                else
-                    hipLaunchKernelGGL((la::gdr_group_kernel<T, DK, DV, la::kGroupScan>), dim3((unsigned)pairs),
-                                       dim3(64 * la::kGroupWaves), 0, c.stream, sa);
-                if (la_status e = hip_check("inter-chunk scan launch")) return e;
-                return launch_out<T, DK, DV>(c, ws, 0, trace);
-            }
-        }
-        if (with_out) {
-            // the scan's output wave produces the output: no output launch
-            hipLaunchKernelGGL((la::gdr_scan1o_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(128), 0,
-                               c.stream, sa);
-            if (la_status e = hip_check("inter-chunk scan launch")) return e;
-            return launch_out<T, DK, DV>(c, ws, 0, trace);
-        }
-        if (scan_variant(sizeof(T) == 4, DK) == 1)
-            hipLaunchKernelGGL((la::gdr_scan1_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(64), 0,
-                               c.stream, sa);
-        else
-            hipLaunchKernelGGL((la::gdr_scan_kernel<T, DK, DV>), dim3((unsigned)blocks),
-                               dim3(64 * la::ScanGeom<DK>::NW), 0, c.stream, sa);
+    trace_mark(1, c.stream);
+    la::ScanArgs sa = scan_args(c, ws);
+    constexpr int NT = DV / 16;
+    const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
+    const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
+    if (prefill_form(s) == LA_FORM_TILE_SCAN_OUT) {
+        // the scan's output wave produces the output: no output launch
+        hipLaunchKernelGGL((la::gdr_scan1o_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(128), 0, c.stream, sa);
         if (la_status e = hip_check("inter-chunk scan launch")) return e;
+        trace_mark(2, c.stream);
+    } else {
+        hipLaunchKernelGGL((la::gdr_scan_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(64 * la::ScanGeom<DK>::NW), 0,
+                           c.stream, sa);
+        if (la_status e = hip_check("inter-chunk scan launch")) return e;
+        trace_mark(2, c.stream);
+        if (max_chunks > 0) {
+            la::OutArgs oa{c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps, (int32_t)max_chunks, s->scale,
+                           ws, chunk_major};
+            const int64_t ob = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
+            hipLaunchKernelGGL((la::gdr_out_kernel<T, DK, DV>), dim3((unsigned)ob), dim3(4 * DV), 0, c.stream, oa);
+            if (la_status e = hip_check("output launch")) return e;
+        }
     }
-    return launch_out<T, DK, DV>(c, ws, max_chunks, trace);
+    trace_mark(3, c.stream);
+    return LA_OK;
 }
 
-template <typename T>
+template <int DK, int DV>
+la_status launch_prefill(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) {
+    if (c.shape->io_dtype == LA_BF16) return launch_fused<DK, DV>(c, p, max_chunks);
+    return launch_f32<DK, DV>(c, p, max_chunks);
+}
+
 la_status dispatch_dims(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) {
     const int dk = c.shape->dk, dv = c.shape->dv;
-    if (dk == 64 && dv == 64) return launch_prefill<T, 64, 64>(c, p, max_chunks);
-    if (dk == 64 && dv == 128) return launch_prefill<T, 64, 128>(c, p, max_chunks);
-    if (dk == 128 && dv == 64) return launch_prefill<T, 128, 64>(c, p, max_chunks);
-    if (dk == 128 && dv == 128) return launch_prefill<T, 128, 128>(c, p, max_chunks);
+    if (dk == 64 && dv == 64) return launch_prefill<64, 64>(c, p, max_chunks);
+    if (dk == 64 && dv == 128) return launch_prefill<64, 128>(c, p, max_chunks);
+    if (dk == 128 && dv == 64) return launch_prefill<128, 64>(c, p, max_chunks);
+    if (dk == 128 && dv == 128) return launch_prefill<128, 128>(c, p, max_chunks);
     return fail(LA_ERR_UNSUPPORTED, "dk=%d dv=%d", dk, dv);
 }
 
@@ -448,7 +352,6 @@ la_status run_prefill(const PrefillCall &c) {
     if (la_status e = check_shape(c.shape)) return e;
     const la_shape *s = c.shape;
     const bool resume = c.start_host != nullptr || c.start_dev != nullptr;
-    if (c.stages == 0 || (c.stages & ~LA_STAGE_ALL)) return fail(LA_ERR_INVALID_ARG, "stages=%u", c.stages);
     if (!resume && c.state_in) return fail(LA_ERR_INVALID_ARG, "state_in given without start positions");
     const int64_t C = s->ckpt_interval;
     const int cps = la::chunks_per_interval(s->ckpt_interval);
@@ -541,8 +444,7 @@ la_status run_prefill(const PrefillCall &c) {
         }
     }
 
-    if (s->io_dtype == LA_BF16) return dispatch_dims<__bf16>(c, p, max_chunks);
-    return dispatch_dims<float>(c, p, max_chunks);
+    return dispatch_dims(c, p, max_chunks);
 }
 
 template <typename T, int DK, int DV>
@@ -745,6 +647,33 @@ size_t la_prefill_workspace_bytes(const la_shape *shape, int64_t total_tokens) {
     return plan_workspace(shape, total_tokens).total;
 }
 
+la_form la_prefill_form(const la_shape *shape) {
+    if (check_shape(shape) != LA_OK) return LA_FORM_NONE;
+    return prefill_form(shape);
+}
+
+la_status la_checkpoint_rows(int32_t n_seqs, const int32_t *cu_seqlens_host, const int64_t *start_pos_host,
+                             int64_t interval, int32_t *offsets_out, int64_t *total_rows_out) {
+    if (n_seqs < 0) return fail(LA_ERR_INVALID_ARG, "n_seqs=%d < 0", n_seqs);
+    if (interval < 1) return fail(LA_ERR_INVALID_ARG, "C=%lld < 1", (long long)interval);
+    if (!total_rows_out || (n_seqs > 0 && (!cu_seqlens_host || !offsets_out)))
+        return fail(LA_ERR_INVALID_ARG, "cu_seqlens_host, offsets_out and total_rows_out are required");
+    int64_t row = 0;
+    for (int i = 0; i < n_seqs; ++i) {
+        const int64_t len = (int64_t)cu_seqlens_host[i + 1] - cu_seqlens_host[i];
+        const int64_t b = start_pos_host ? start_pos_host[i] : 0;
+        if (len < 0) return fail(LA_ERR_INVALID_ARG, "cu_seqlens decreases at sequence %d", i);
+        if (b < 0 || b > ((int64_t)1 << 40)) return fail(LA_ERR_INVALID_ARG, "start_pos[%d]=%lld", i, (long long)b);
+        if (row > 0x7fffffff) return fail(LA_ERR_INVALID_ARG, "more than 2^31 checkpoint rows");
+        offsets_out[i] = (int32_t)row;
+        // checkpoints at the absolute multiples of C in (B_i, B_i + len_i]
+        row += (b + len) / interval - b / interval;
+    }
+    if (row > 0x7fffffff) return fail(LA_ERR_INVALID_ARG, "more than 2^31 checkpoint rows");
+    *total_rows_out = row;
+    return LA_OK;
+}
+
 la_status la_prefill(const la_shape *shape, const void *q, const void *k, const void *v, const float *g,
                      const float *beta, const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host, void *o,
                      float *final_state, float *ckpt_out, const int32_t *ckpt_offsets_dev,
@@ -768,20 +697,6 @@ la_status la_prefill_resume(const la_shape *shape, const void *q, const void *k,
     return run_prefill(c);
 }
 
-la_status la_prefill_stages(const la_shape *shape, uint32_t stages, const void *q, const void *k, const void *v,
-                            const float *g, const float *beta, const int32_t *cu_seqlens_dev,
-                            const int32_t *cu_seqlens_host, const int64_t *start_pos_dev,
-                            const int64_t *start_pos_host, const float *state_in, void *o, float *final_state,
-                            float *ckpt_out, const int32_t *ckpt_offsets_dev, const int32_t *ckpt_offsets_host,
-                            void *workspace, size_t ws_bytes, void *stream) {
-    if ((start_pos_dev == nullptr) != (start_pos_host == nullptr))
-        return fail(LA_ERR_INVALID_ARG, "start_pos_dev and start_pos_host go together");
-    PrefillCall c{shape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host, start_pos_dev, start_pos_host,
-                  state_in, o, final_state, ckpt_out, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
-                  (hipStream_t)stream, stages};
-    return run_prefill(c);
-}
-
 la_status la_prefill_paged(const la_shape *shape, const la_pages *pages, const void *q, const void *k, const void *v,
                            const float *g, const float *beta, const int32_t *cu_seqlens_dev,
                            const int32_t *cu_seqlens_host, const int64_t *start_pos_dev,
@@ -793,7 +708,7 @@ la_status la_prefill_paged(const la_shape *shape, const la_pages *pages, const v
         return fail(LA_ERR_INVALID_ARG, "start_pos_dev and start_pos_host go together");
     PrefillCall c{shape, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host, start_pos_dev, start_pos_host,
                   nullptr, o, final_state, nullptr, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
-                  (hipStream_t)stream, LA_STAGE_ALL, pages};
+                  (hipStream_t)stream, pages};
     return run_prefill(c);
 }
 

@@ -32,7 +32,7 @@ LA_GDR_LITERAL = 0
 LA_GDR_DECAYED_DELTA = 1
 
 EXPORTED = ("strict_prefix_boundary", "la_prefill_workspace_bytes", "la_prefill",
-            "la_prefill_resume", "la_prefill_stages", "la_prefill_paged", "la_decode_step", "la_state_save_paged",
+            "la_prefill_resume", "la_checkpoint_rows", "la_prefill_form", "la_prefill_paged", "la_decode_step", "la_state_save_paged",
             "la_state_restore_paged",
             "la_state_save_host", "la_state_restore_host", "la_hybrid_boundary", "la_hybrid_restore",
             "la_status_string", "la_last_error_message", "la_trace_set_events")
@@ -87,7 +87,8 @@ def _load() -> ctypes.CDLL:
         "la_prefill_workspace_bytes": ([SH, I64], SZ),
         "la_prefill": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_prefill_resume": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
-        "la_prefill_stages": ([SH, ctypes.c_uint32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "la_checkpoint_rows": ([I32, P, P, I64, P, ctypes.POINTER(I64)], I32),
+        "la_prefill_form": ([SH], I32),
         "la_prefill_paged": ([SH, ctypes.POINTER(LaPages), P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_decode_step": ([SH, P, P, P, P, P, P, P, P], I32),
         "la_state_save_paged": ([P, I64, I64, P, I64, P, P, P], I32),
@@ -234,25 +235,25 @@ def la_state_restore_paged(pool, page_ids_dev, states, err_count_dev=None, strea
     return st
 
 
-LA_STAGE_PREPARE, LA_STAGE_SCAN, LA_STAGE_OUTPUT, LA_STAGE_ALL = 1, 2, 4, 7
+LA_FORM_NONE, LA_FORM_FUSED_SCAN, LA_FORM_FUSED_TWO_LEVEL, LA_FORM_TILE_SCAN_OUT, LA_FORM_SPLIT_DK_SCAN = 0, 1, 2, 3, 4
 
 
-def la_prefill_stages(shape: LaShape, stages: int, q, k, v, g, beta, cu_dev, cu_host, start_dev, start_host,
-                      state_in, o, final_state, ckpt_out, ckpt_off_dev, ckpt_off_host, workspace, stream=None,
-                      check: bool = True) -> int:
-    """A subset of one prefill call's stages (mask of LA_STAGE_*); start_dev /
-    start_host None make it a cold call."""
-    cu_host = np.ascontiguousarray(cu_host, dtype=np.int32)
-    sh = None if start_host is None else np.ascontiguousarray(start_host, dtype=np.int64)
-    oh = None if ckpt_off_host is None else np.ascontiguousarray(ckpt_off_host, dtype=np.int32)
-    st = _lib.la_prefill_stages(ctypes.byref(shape), stages, _dptr(q), _dptr(k), _dptr(v), _dptr(g), _dptr(beta),
-                                _dptr(cu_dev), _hptr(cu_host, np.int32), _dptr(start_dev),
-                                _hptr(sh, np.int64), _dptr(state_in), _dptr(o), _dptr(final_state),
-                                _dptr(ckpt_out), _dptr(ckpt_off_dev), _hptr(oh, np.int32), _dptr(workspace),
-                                workspace.numel() * workspace.element_size(), _stream(stream))
-    if check:
-        _check(st)
-    return st
+def la_prefill_form(shape: LaShape) -> int:
+    """Which kernels a prefill of this shape runs (LA_FORM_*)."""
+    return _lib.la_prefill_form(ctypes.byref(shape))
+
+
+def la_checkpoint_rows(cu_seqlens_host, start_pos_host, interval: int):
+    """Checkpoint row offsets per sequence and the total row count, as the
+    library numbers them (start_pos_host None: a cold call)."""
+    cu = np.ascontiguousarray(cu_seqlens_host, dtype=np.int32)
+    n = len(cu) - 1
+    sp = None if start_pos_host is None else np.ascontiguousarray(start_pos_host, dtype=np.int64)
+    offs = np.zeros(max(n, 0), np.int32)
+    total = ctypes.c_int64(-1)
+    _check(_lib.la_checkpoint_rows(n, _hptr(cu, np.int32), _hptr(sp, np.int64), int(interval),
+                                   _hptr(offs, np.int32), ctypes.byref(total)))
+    return offs, total.value
 
 
 def make_pages(pool, ckpt_page_ids=None, state_page_ids=None, err_count=None, n_pages=None) -> LaPages:

@@ -75,12 +75,8 @@ def test_workspace_bytes():
     a = la.la_prefill_workspace_bytes(sh, 3584)
     b = la.la_prefill_workspace_bytes(sh, 7168)
     assert 0 < a < b
-    # 56 chunks x 8 heads x (W, K~^T, S_0, U in bf16; U~, G in fp32)
-    per = 64 * 128 * 2 * 2 + 64 * 128 * 4 + 64 * 4 + 128 * 128 * 2 + 64 * 128 * 2
-    assert a >= 56 * 8 * per
-    assert la.la_prefill_workspace_bytes(la.make_shape(1, 8, 96, 128, 256), 100) == 0
-    assert la.la_prefill_workspace_bytes(la.make_shape(1, 8, 128, 128, 256, chunk=32), 100) == 0
-    assert la.la_prefill_workspace_bytes(la.make_shape(1, 8, 128, 128, 0), 100) == 0
+    # 56 chunks x 8 heads x (X fragments 6 KB + gate block 1 KB)
+    assert a >= 56 * 8 * 7 * 1024
 
 
 FAKE = 1 << 20          # 16-byte aligned dummy device address (never dereferenced)
@@ -133,24 +129,85 @@ def test_paged_validation_before_launch():
     assert lib.la_state_save_paged(FAKE, 0, 8, FAKE, 8, FAKE, None, None) == la.LA_OK   # nothing to do
 
 
-def test_stage_mask_validation_before_launch():
+def test_resume_state_validation_before_launch():
     lib = la.library()
     sh = la.make_shape(1, 1, 64, 64, 16)
     cu = np.array([0, 64], np.int32)
     P = la.ctypes.c_void_p
     ws = lib.la_prefill_workspace_bytes(la.ctypes.byref(sh), 64)
 
-    def call(stages, state_in=None, starts=None):
-        st = None if starts is None else np.asarray(starts, np.int64)
-        return lib.la_prefill_stages(la.ctypes.byref(sh), stages, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                     P(cu.ctypes.data), FAKE if st is not None else None,
-                                     P(st.ctypes.data) if st is not None else None, state_in, FAKE, FAKE,
-                                     None, None, None, FAKE, ws, None)
-    assert call(0) == la.LA_ERR_INVALID_ARG
-    assert call(8) == la.LA_ERR_INVALID_ARG
-    assert call(la.LA_STAGE_ALL, state_in=FAKE) == la.LA_ERR_INVALID_ARG      # a state without positions
-    assert call(la.LA_STAGE_PREPARE, starts=[16]) == la.LA_ERR_INVALID_ARG    # resume without a state
-    assert call(la.LA_STAGE_SCAN, state_in=FAKE, starts=[8]) == la.LA_ERR_MISALIGNED_STATE
+    def call(state_in=None, starts=(16,)):
+        st = np.asarray(starts, np.int64)
+        return lib.la_prefill_resume(la.ctypes.byref(sh), FAKE, FAKE, FAKE, FAKE, FAKE, P(cu.ctypes.data),
+                                     P(cu.ctypes.data), FAKE, P(st.ctypes.data), state_in, FAKE, FAKE, None,
+                                     None, None, FAKE, ws, None)
+    assert call(state_in=None) == la.LA_ERR_INVALID_ARG                  # resume without a state
+    assert call(state_in=FAKE, starts=[8]) == la.LA_ERR_MISALIGNED_STATE
+    assert call(state_in=FAKE + 4) == la.LA_ERR_INVALID_ARG              # misaligned state
+
+
+def test_prefill_form_is_a_function_of_the_shape():
+    """The kernels a call runs depend on dtype, head dims and C only (never
+    on lengths), so a resume runs the arithmetic of the run that wrote its
+    checkpoint: bf16 takes the fused scan, or the two-level fused scan from
+    C > 448 (8 chunks per interval); fp32 the one-tile scan with its output
+    wave (dk = 64) or the dk-split scan (dk = 128)."""
+    F = la.la_prefill_form
+    for d in (64, 128):
+        for C in (16, 64, 256, 448):
+            assert F(la.make_shape(3, 8, d, 128, C, la.LA_BF16)) == la.LA_FORM_FUSED_SCAN
+        for C in (449, 512, 1024, 1792):
+            assert F(la.make_shape(3, 8, d, 128, C, la.LA_BF16)) == la.LA_FORM_FUSED_TWO_LEVEL
+    assert F(la.make_shape(1, 1, 64, 64, 16, la.LA_F32)) == la.LA_FORM_TILE_SCAN_OUT
+    assert F(la.make_shape(1, 1, 64, 128, 1024, la.LA_F32)) == la.LA_FORM_TILE_SCAN_OUT
+    assert F(la.make_shape(1, 1, 128, 64, 16, la.LA_F32)) == la.LA_FORM_SPLIT_DK_SCAN
+    assert F(la.make_shape(1, 1, 96, 128, 16)) == la.LA_FORM_NONE
+
+
+def test_checkpoint_rows_match_absolute_multiples():
+    """la_checkpoint_rows numbers the multiples of C in (B_i, B_i + len_i]
+    consecutively, sequence after sequence (brute force over positions)."""
+    rng = np.random.default_rng(7)
+    for _ in range(200):
+        n = int(rng.integers(1, 9))
+        C = int(rng.choice([1, 16, 64, 256, 1792]))
+        lens = rng.integers(0, 5 * C + 3, n)
+        starts = None if rng.random() < 0.3 else C * rng.integers(0, 6, n)
+        cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        offs, total = la.la_checkpoint_rows(cu, starts, C)
+        row = 0
+        for i in range(n):
+            b = 0 if starts is None else int(starts[i])
+            assert offs[i] == row
+            row += sum(1 for p in range(b + 1, b + int(lens[i]) + 1) if p % C == 0)
+        assert total == row
+    with pytest.raises(la.LinAttnError):
+        la.la_checkpoint_rows(np.array([0, 5, 3], np.int32), None, 16)
+    with pytest.raises(la.LinAttnError):
+        la.la_checkpoint_rows(np.array([0, 5], np.int32), None, 0)
+
+
+def test_workspace_holds_only_what_the_form_uses():
+    """bf16 calls keep 7 KB per chunk slot and head (X fragments and the
+    gate block), plus the segment regions of the two-level scan; fp32 calls
+    keep the per-chunk operands, and the dk-split form also the per-chunk
+    states and U its output kernel reads."""
+    def ws(n_seqs, H, dk, dv, C, io, tokens):
+        return la.la_prefill_workspace_bytes(la.make_shape(n_seqs, H, dk, dv, C, io), tokens)
+    # varlen batch: 16 sequences, 77,456 tokens, 8 heads, C = 256 (1,217 chunk slots at most)
+    slots = (77456 + 255 * 16) // 256 * 4
+    got = ws(16, 8, 128, 128, 256, la.LA_BF16, 77456)
+    assert got <= slots * 8 * (6 * 1024 + 1024) + 4096
+    assert got < 0.1 * 1.15 * 2 ** 30            # the operand workspace of the unfused path was 1.15 GiB
+    # two-level (C = 1024, 16 chunks per segment): + Phi' (bf16) + R + D + entering state per segment-head
+    one = ws(1, 16, 128, 128, 1024, la.LA_BF16, 32768)
+    segs = 32 * 16
+    assert one >= 512 * 16 * 7 * 1024 + segs * (128 * 128 * 2 + 2 * 128 * 128 * 4)
+    # fp32 forms: the split-dk scan needs the per-chunk states and U, the one-tile form does not
+    a64 = ws(1, 1, 64, 64, 16, la.LA_F32, 256)
+    a128 = ws(1, 1, 128, 64, 16, la.LA_F32, 256)
+    slots32 = 16
+    assert a128 - a64 >= slots32 * (128 * 64 * 4 + 64 * 64 * 4)
 
 
 def test_paged_prefill_validation_before_launch():

@@ -195,11 +195,10 @@ def test_prefix_double_application_is_detected():
     assert state_err(host(good.final_state), fin_ref) <= TOL[la.LA_BF16]
 
 
-def test_many_chains_workgroup_scan():
-    """A batch of 320 (sequence, head) chains, 2,560 column tiles: more than
-    the per-tile scan with output wave takes, so the scan runs one workgroup
-    per chain with output waves beside it.  Parity with the oracle; a
-    sequence alone (per-tile scan) gives the same bits as inside the batch;
+def test_many_chains_in_several_rounds():
+    """A batch of 320 (sequence, head) chains: more fused-scan workgroups
+    than CUs, so they run in several rounds.  Parity with the oracle on
+    every head; a sequence alone gives the same bits as inside the batch;
     and every sequence resumed at its strict-prefix boundary from the
     batch's own checkpoints reproduces the cold run's tail and final state
     bit for bit."""
@@ -209,7 +208,7 @@ def test_many_chains_workgroup_scan():
     x = wl.random_inputs(511, lens, H, 128, 128, wl.BF16)
     xd, res = _run_cold(x, C)
     ref = oracle_run(x, interval=C)
-    compare(res, ref, x.cu_seqlens, TOL[la.LA_BF16], "40 seqs x 8 heads, workgroup scan")
+    compare(res, ref, x.cu_seqlens, TOL[la.LA_BF16], "40 seqs x 8 heads, several rounds")
     cu = x.cu_seqlens
     i = int(np.argmax(lens))
     alone = api.prefill(api.to_device(x.seq(i)), C)
@@ -234,21 +233,43 @@ def test_many_chains_workgroup_scan():
     assert torch.equal(r2.final_state, res.final_state)
 
 
-@pytest.mark.parametrize("dk,dv", [(64, 64), (64, 128), (128, 64)])
-def test_pair_tile_scan_head_dims(dk, dv):
-    """33 sequences x 8 heads: more one-tile scan workgroups than are
-    resident at once, so the scan with output wave runs over pairs of column
-    tiles.  Parity with the oracle, and a sequence alone (one-tile kernel)
-    gives the same bits as inside the batch."""
+@pytest.mark.parametrize("dk,dv", [(64, 64), (64, 128), (128, 64), (128, 128)])
+def test_fused_scan_batch_head_dims(dk, dv):
+    """33 sequences x 8 heads for every built head-dimension pair, on the
+    fused scan (the form is asserted): parity with the oracle on every head,
+    and a sequence alone gives the same bits as inside the batch."""
     rng = np.random.default_rng(600 + dk + dv)
     lens = [int(n) for n in rng.integers(64, 700, size=33)]
     C = 128
     x = wl.random_inputs(600 + dk + dv, lens, 8, dk, dv, wl.BF16)
+    assert la.la_prefill_form(la.make_shape(33, 8, dk, dv, C)) == la.LA_FORM_FUSED_SCAN
     xd, res = _run_cold(x, C)
     ref = oracle_run(x, interval=C)
-    compare(res, ref, x.cu_seqlens, TOL[la.LA_BF16], f"33 seqs x 8 heads dk={dk} dv={dv}, pair-tile scan")
+    compare(res, ref, x.cu_seqlens, TOL[la.LA_BF16], f"33 seqs x 8 heads dk={dk} dv={dv}, fused scan")
     i = int(np.argmax(lens))
     alone = api.prefill(api.to_device(x.seq(i)), C)
     torch.cuda.synchronize()
     s, e = int(x.cu_seqlens[i]), int(x.cu_seqlens[i + 1])
     assert torch.equal(alone.o, res.o[s:e]) and torch.equal(alone.final_state[0], res.final_state[i])
+
+
+@pytest.mark.parametrize("dk,dv", [(64, 64), (128, 64), (128, 128)])
+def test_two_level_head_dims(dk, dv):
+    """The two-level fused scan (C = 512: 8 chunks per interval, segments of
+    8 chunks) for head-dimension pairs that split the map's columns
+    differently: parity on every head, and a resume from the run's own
+    checkpoint reproduces its tail bit for bit."""
+    lens = [1500, 700, 2048]
+    C = 512
+    x = wl.random_inputs(620 + dk + dv, lens, 3, dk, dv, wl.BF16)
+    assert la.la_prefill_form(la.make_shape(3, 3, dk, dv, C)) == la.LA_FORM_FUSED_TWO_LEVEL
+    xd, res = _run_cold(x, C)
+    ref = oracle_run(x, interval=C)
+    compare(res, ref, x.cu_seqlens, TOL[la.LA_BF16], f"two-level dk={dk} dv={dv}")
+    i, B = 2, 1536
+    xs = api.to_device(x.seq(i).tokens(B, lens[i]))
+    off = int(res.ckpt_offsets[i])
+    r2 = api.prefill_resume(xs, [B], res.ckpt[off + B // C - 1:off + B // C].clone(), C)
+    torch.cuda.synchronize()
+    s = int(x.cu_seqlens[i])
+    assert torch.equal(r2.o, res.o[s + B:s + lens[i]]) and torch.equal(r2.final_state[0], res.final_state[i])
