@@ -190,33 +190,6 @@ __device__ inline void store_state_tiles(float *dst, const f32x4 (&S)[NTILE], ui
                                                   (16 * t + i) * DV * (int)sizeof(float), 0);
 }
 
-// Row-major store of NTILE 16-row tiles of one 16-column state tile through a
-// per-wave LDS transpose: each lane writes 16 bytes (4 consecutive columns of
-// one row) per store instead of one dword per row, so a [DK, 16] tile takes
-// DK/16 vector stores.  dst points at (row 0, the tile's first column) of a
-// row-major block with DV columns; lds holds NTILE * 16 * kTrLd floats owned
-// by this wave (the padded row keeps the 16-byte reads aligned and the
-// column writes conflict-free).
-constexpr int kTrLd = 20;
-
-template <int NTILE, int DV>
-__device__ inline void store_state_tiles_t(float *dst, const f32x4 (&S)[NTILE], float *lds) {
-    const int lane = threadIdx.x & 63, g16 = lane >> 4, c16 = lane & 15;
-#pragma unroll
-    for (int t = 0; t < NTILE; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) lds[(16 * t + 4 * g16 + i) * kTrLd + c16] = S[t][i];
-    const auto r = make_rsrc(dst, (uint32_t)(((NTILE * 16 - 1) * DV + 16) * sizeof(float)));
-    const int rr = lane >> 2, cc = 4 * (lane & 3);
-    const uint32_t voff = (uint32_t)((rr * DV + cc) * sizeof(float));
-#pragma unroll
-    for (int p = 0; p < NTILE; ++p) {
-        const float4 v = *(const float4 *)&lds[(16 * p + rr) * kTrLd + cc];
-        buf_store16(make_uint4(__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)),
-                    r, voff, (uint32_t)(16 * p * DV * sizeof(float)));
-    }
-}
-
 // State tiles in C layout ([tile][row tile][lane] of f32x4): the two-level
 // scan's segment-entering states, written by the combine and read by the
 // replay (one 16-byte access per row tile and lane).
@@ -678,99 +651,6 @@ __global__ __launch_bounds__(128) void gdr_scan1o_kernel(ScanArgs a) {
     } else {
         out_wave_chunks<T, DK, DV>(a, h, tile, cu0, len, base, nch, &hs);
     }
-}
-
-// Position in the A-operand column order of column c of a [DK][DK] matrix:
-// A-operand k-step ks of a lane in group g takes columns perm_row(8 ks + j, g)
-// for j < 8, stored contiguously at 32 ks + 8 g + j.
-__device__ inline int phi_col_pos(int c) {
-    const int t = c >> 4, g = (c >> 2) & 3, q = c & 3;
-    return 32 * (t >> 1) + 8 * g + 4 * (t & 1) + q;
-}
-
-// Two-level scan, second level: per (sequence, head, 16-column tile), the
-// segment states in order, S <- D S + Phi' S + R.  The large D I part stays
-// in fp32; only Phi' S goes through the io-type MFMA.  Writes the
-// checkpoints (segment ends on a multiple of C), the entering state of every
-// later segment, and the final state.
-template <typename T, int DK, int DV>
-__global__ __launch_bounds__(64) void gdr_seg_combine_kernel(ScanArgs a) {
-    using M = MT<T>;
-    constexpr int KW = M::KW, VEC = Vec<T>::N;
-    constexpr int RT = DK / 16, NT = DV / 16;
-    constexpr int FS = DK / 4, VS = FS / VEC;
-    constexpr int kMfmas = RT * (FS / KW), kLoads = 1 + RT + RT * VS;
-    const int lane = threadIdx.x, g16 = lane >> 4, c16 = lane & 15;
-    const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
-    const int pair = chain_of_rank(a, xcd + 8 * (q / NT)), tile = q % NT;
-    const int H = a.n_heads;
-    if (pair < 0) return;
-    const int seq = pair / H, h = pair % H;
-    const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
-    const int nch = n_chunks32(len, a.C, a.cps);
-    const int nseg = (nch + a.seg_m - 1) / a.seg_m;
-    const int64_t sbase = slot_base_dev(cu0, seq, (int64_t)a.C * a.seg_m, a.cps);
-    const size_t state_off = (size_t)pair * DK * DV;
-    __shared__ float tr_lds[DK * kTrLd];
-    f32x4 S[RT];
-    load_state_tile<DK, DV>(start_state(a, seq, h, (size_t)DK * DV, tile == 0), tile, S);
-    CkptDst ck;
-    ck.init(a, seq, h, len, (size_t)DK * DV, tile == 0);
-    const uint32_t lane16 = 16u * (uint32_t)lane;
-    const uint32_t phi_lane = (uint32_t)((c16 * DK + 8 * g16) * sizeof(T));
-    __builtin_amdgcn_s_waitcnt(0);
-
-    struct Ops {
-        float d;
-        int ckid;             // page id of the checkpoint this segment would end (paged)
-        f32x4 r[RT];
-        uint4 ph[RT][VS];
-    };
-    auto load = [&](Ops &o, int sg) {
-        const int64_t ssh = (sbase + sg) * H + h;
-        o.ckid = ck.load_id(max((sg + 1) * a.seg_m / a.cps - 1, 0));
-        o.d = buf_load4f(make_rsrc(a.seg.d + ssh, sizeof(float)), 0u, 0u);
-        const auto rr = make_rsrc(a.seg.r + ssh * DK * DV, DK * DV * sizeof(float));
-#pragma unroll
-        for (int t = 0; t < RT; ++t) {
-            const uint4 x = buf_load16(rr, lane16, 1024u * (tile * RT + t));
-            o.r[t] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
-        }
-        const auto rp = make_rsrc((const T *)a.seg.phi + ssh * DK * DK, DK * DK * sizeof(T));
-#pragma unroll
-        for (int t = 0; t < RT; ++t)
-#pragma unroll
-            for (int v = 0; v < VS; ++v)
-                o.ph[t][v] = buf_load16(rp, phi_lane, (uint32_t)((16 * t * DK + v * VEC * 4) * sizeof(T)));
-    };
-    auto step = [&](const Ops &o, int sg) {
-        T sb[FS];
-#pragma unroll
-        for (int f = 0; f < FS; ++f) sb[f] = from_f32<T>(S[f >> 2][f & 3]);
-#pragma unroll
-        for (int t = 0; t < RT; ++t) {
-            const T *pv = (const T *)&o.ph[t][0];
-            f32x4 acc = S[t] * o.d + o.r[t];
-#pragma unroll
-            for (int ks = 0; ks < FS / KW; ++ks)
-                acc = M::mma(M::pack(&pv[ks * KW]), M::pack(&sb[ks * KW]), acc);
-            S[t] = acc;
-        }
-#pragma unroll
-        for (int i = 0; i < kMfmas; ++i) {
-            if (i < kLoads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        }
-        if (kLoads > kMfmas) __builtin_amdgcn_sched_group_barrier(0x020, kLoads - kMfmas, 0);
-        int lo, hi;
-        chunk_range32(min((sg + 1) * a.seg_m, nch) - 1, len, a.C, a.cps, &lo, &hi);
-        if (sg + 1 < nseg) store_state_c<RT>(a.seg.state + ((sbase + sg + 1) * H + h) * DK * DV, tile, S);
-        if (hi % a.C == 0) {   // checkpoints come in order, one per C-aligned segment end
-            if (float *d = ck.next(o.ckid)) store_state_tiles_t<RT, DV>(d + 16 * tile, S, tr_lds);
-        }
-    };
-    scan_ring<1>(nseg, load, step, (Ops *)nullptr);
-    if (a.final_state) store_state_tiles_t<RT, DV>(a.final_state + state_off + 16 * tile, S, tr_lds);
 }
 
 }  // namespace la

@@ -21,6 +21,8 @@
 //     j < 8.  X is lower triangular, so only k-steps ks <= mt / 2 are stored
 //     (6 fragments of 1 KB: slot xfrag_slot(mt, ks));
 //   the gate block: G, d = beta exp(Gp), beta and exp(G_63 - G), 64 fp32 each.
+// Both sit in one 7 KB block per chunk-head (X fragments, then the gate
+// block), which the scan copies into LDS as is.
 // Every exponent is a difference formed before exponentiation (<= 0 when
 // g <= 0): no exp(-G) factor is ever formed.
 #pragma once
@@ -30,6 +32,7 @@ namespace la {
 
 constexpr int kXFrags = 6;                     // stored X fragments per chunk-head
 constexpr int kGateBlock = 4 * kChunk;         // floats of the gate block per chunk-head
+constexpr int kMiscVec = kXFrags * 64 + kGateBlock / 4;   // 16-byte vectors per chunk-head block (7 KB)
 
 __device__ __host__ inline int xfrag_slot(int mt, int ks) { return mt < 2 ? mt : 2 * mt - 2 + ks; }
 
@@ -38,8 +41,8 @@ struct XPrepArgs {
     const float *g, *beta;
     const int32_t *cu;
     int32_t n_seqs, n_heads, C, cps, variant, max_chunks;
-    void *xf;          // X fragments [slot-head][kXFrags][64 lanes] x 16 B
-    float *gb;         // gate blocks [slot-head][4][64]: G, d, beta, exp(G_63 - G)
+    uint4 *misc;       // per slot-head: X fragments [kXFrags][64 lanes] x 16 B, then
+                       // the gate block [4][64] fp32: G, d, beta, exp(G_63 - G)
     int32_t chunk_major;
 };
 
@@ -114,7 +117,7 @@ __global__ __launch_bounds__(256) void gdr_xprep_kernel(XPrepArgs a) {
             sm.G2[lane] = x * kLog2e;
             sm.Gp2[lane] = gp * kLog2e;
             sm.bs[lane] = b;
-            float *gb = a.gb + sh * kGateBlock;
+            float *gb = (float *)(a.misc + sh * kMiscVec + kXFrags * 64);
             gb[lane] = x;
             gb[kChunk + lane] = b * __builtin_amdgcn_exp2f(gp * kLog2e);
             gb[2 * kChunk + lane] = b;
@@ -211,7 +214,7 @@ __global__ __launch_bounds__(256) void gdr_xprep_kernel(XPrepArgs a) {
     // above the diagonal are zeroed here (the LDS there is stale).
     {
         const int mt = wave, r = 16 * mt + c16;
-        uint4 *xout = (uint4 *)a.xf + sh * (kXFrags * 64);
+        uint4 *xout = a.misc + sh * kMiscVec;
         for (int ks = 0; ks <= (mt >> 1); ++ks) {
             __bf16 v8[8];
 #pragma unroll

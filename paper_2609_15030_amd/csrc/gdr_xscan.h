@@ -3,30 +3,39 @@
 // workgroup in LDS.
 //
 // A workgroup owns CW state columns of one (sequence, head) and runs its
-// chunks in order; its CW / 32 waves own 32 columns (two 16-column tiles)
-// each and keep them in fp32 MFMA result registers (C layout: lane (g, c)
-// holds rows 4 g + i of every 16-row tile, column c).  Per chunk, with S_0
-// the state entering it and the gate block and X written by the
-// preparation kernel (gdr_xprep.h):
+// chunks in order.  Each 32 of its columns (two 16-column tiles) belong to
+// a pair of waves on one SIMD: a scan wave, which keeps those columns of the
+// fp32 state in MFMA result registers for the whole run, and (when the unit
+// has an output) an output wave, which reads the output out beside it and
+// fills the scan wave's stalls.  Per chunk, with S_0 the state entering it
+// and the gate block and X written by the preparation kernel (gdr_xprep.h):
 //
-//   Y  = K S_0                           A = K rows, B = S_0 (k = dk, perm_row)
-//   Z  = diag(beta) V - diag(d) Y        d = beta exp(Gp), V read in C layout
-//   U  = X Z                             A = X fragments, B = Z (k = chunk rows)
-//   S_1 = exp(G_63) S_0 + K^T diag(exp(G_63 - G)) U
-//                                        A = K^T (transposed LDS reads), B = U
-//   O^T = scale ((S_0^T Q^T) diag(exp G) + U^T P^T)
-//        P = (Q K^T) exp(G_r - G_s) on s <= r, zero above
+//   scan wave    Y   = K S_0                      A = K rows, B = S_0
+//                Z   = diag(beta) V - diag(d) Y   d = beta exp(Gp), V in C layout
+//                U   = X Z                        A = X fragments, B = Z
+//                S_1 = exp(G_63) S_0 + K^T diag(exp(G_63 - G)) U
+//   output wave  O^T = scale ((S_0^T Q^T) diag(exp G) + U^T P^T),
+//                P   = (Q K^T) exp(G_r - G_s) on s <= r, zero above
+//                      (tiles dealt over the output waves, shared in LDS)
 //
-// The products take their operands straight from registers: a C-layout
-// result read with the contraction index permuted by perm_row is a B
-// operand over its rows, and, transposed, an A operand over its rows.  So
-// S_0 (as B of Y and A of S_0^T Q^T), Z, and U (as B of the state update and
-// A of U^T P^T) never move between lanes.  K and Q are staged twice over
-// where needed: with their dk columns permuted (phi_col_pos) so that an
-// A-operand fragment of K or Q is one 16-byte LDS read, and K also in
-// natural order for the transposed reads of K^T.  The P tiles are computed
-// as K Q^T, whose accumulator layout is the P operand's, split over the
-// waves and shared through LDS.
+// Operands stay in the lanes that produce them: a C-layout result read with
+// the contraction index permuted by perm_row is a B operand over its rows,
+// and, transposed, an A operand over its rows.  The state's rows are held in
+// a fixed permutation of dk (state_row): then the contraction order in which
+// S_0 enters Y = K S_0 is plain dk order, so an A-operand fragment of K or Q
+// is one 16-byte LDS read of a row, and the fragments of K^T (whose rows must
+// follow the state's) are transposed LDS reads whose per-lane column
+// addresses apply the same permutation.  The state handed to the output wave
+// (S_0 as bf16 B-operand fragments) and U pass through LDS.
+//
+// Loads: the second wave of each pair (the output wave, or in the map a
+// loader wave) stages every chunk's K, Q, values and the preparation's
+// block (X, gates) one chunk ahead: buffer loads into registers while the
+// chunk before is computed, rows past a chunk's end reading as zero through
+// the buffer range, then LDS stores into the other of two buffers.  The scan
+// waves issue no global loads, so no LDS read of theirs waits on one.
+// (Loads with an LDS destination would save the registers, but every LDS
+// read after them would wait for them to land.)
 //
 // Modes (unit = one workgroup):
 //   kXScan    (sequence, head, column part): the whole sequence from its
@@ -48,69 +57,129 @@ namespace la {
 
 enum : int { kXScan = 0, kXReplay = 1, kXMap = 2 };
 
-// Columns per workgroup: a whole 128-column head on four waves; 64 columns
-// on two waves when a head dimension is 64 (the map's Phi and R parts then
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// Columns per workgroup: a whole 128-column head on four wave pairs; 64
+// columns on two when a head dimension is 64 (the map's Phi and R parts then
 // split at a part boundary).
 template <int DK, int DV> constexpr int xscan_cols() { return (DK == 128 && DV == 128) ? 128 : 64; }
+template <int DK, int DV> constexpr int xscan_threads() { return 64 * (xscan_cols<DK, DV>() / 32) * 2; }
 
-template <int DK, int CW> struct XLds {
-    static constexpr int LDP = DK + 8;   // bf16 row pitch, K and Q with permuted dk columns
-    static constexpr int LDN = DK + 8;   // bf16 row pitch, K in natural order (transposed reads)
-    static constexpr int LDV = CW + 8;   // bf16 row pitch, V
-    struct Buf {
-        __bf16 kp[kChunk][LDP];
-        __bf16 kn[kChunk][LDN];
-        __bf16 qp[kChunk][LDP];
-        __bf16 v[kChunk][LDV];
-        uint4 xf[kXFrags][64];
-        float gb[kGateBlock];
-    };
-    Buf buf[2];
-    uint4 pf[4][2][64];   // P fragments [row tile][k-step][lane]
-};
-
-// Position of dk column d in the permuted rows: A-operand k-step ks of lane
-// group g takes columns perm_row(8 ks + j, g), j < 8, which sit at
-// 32 ks + 8 g + j.
-__device__ inline int xperm_pos8(int m) {
-    // start of the first 4-run of the 8 columns 8m .. 8m + 7 (the second
-    // run sits 8 further on)
-    return 32 * (m >> 2) + 16 * (m & 1) + 4 * ((m >> 1) & 1);
+// dk row held at state tile-row x = 16 t + 4 g + q (lane group g, element
+// q of tile t): the B-operand contraction index 8 ks + j of lane group g
+// (perm_row) then stands for dk 32 ks + 8 g + j, plain order.  A lane holds
+// the 8 consecutive dk rows 32 (t / 2) + 8 g .. + 7 across tiles t and t ^ 1.
+__device__ __host__ inline int state_row(int x) {
+    const int t = x >> 4, g = (x >> 2) & 3, q = x & 3;
+    return 32 * (t >> 1) + 8 * g + 4 * (t & 1) + q;
 }
 
-// A-operand fragment of K^T for dk rows [n0, n0 + 16) and k-step ks, the
-// chunk rows permuted by perm_row: lane (g, r) takes K[perm_row(8 ks + j, g)][n0 + r],
-// two runs of 4 rows (32 ks + 4 g and 32 ks + 16 + 4 g), each one transposed
-// LDS read from the natural-order rows.
-__device__ inline bf16x8 kt_frag(const __bf16 *kn, int ld, int ks, int n0, int lane) {
+template <int DK, int CW, bool OUT> struct XLds {
+    static constexpr int NPAIR = CW / 32;
+    static constexpr int KV = kChunk * DK / 8;   // 16-byte pieces of a chunk's K (or Q)
+    struct Buf {
+        uint4 k[KV];                             // K rows, pieces XOR-swizzled by row (xpiece)
+        uint4 q[OUT ? KV : 1];                   // Q, same layout
+        uint4 misc[kMiscVec];                    // X fragments, then the gate block
+    };
+    Buf buf[2];
+    uint4 v[NPAIR][kChunk * 32 / 8];             // each pair's 32 value columns, row-major [64][32]
+    uint4 pf[OUT ? 4 * 2 * 64 : 1];              // P fragments [row tile][k-step][lane]
+    uint4 sbh[OUT ? NPAIR : 1][2][DK / 32][64];  // S_0 handed to the output wave (B-operand fragments)
+    uint4 ubh[OUT ? NPAIR : 1][2][2][64];        // U handed to the output wave
+};
+
+// Physical 16-byte piece of logical piece p in row r of a K or Q tile (DK / 8
+// pieces per row): the XOR swizzle spreads the rows of a fragment read over
+// the LDS banks.
+template <int DK> __device__ inline int xpiece(int r, int p) { return p ^ (r & (DK / 8 - 1)); }
+
+// A-operand fragment of rows [16 mt, 16 mt + 16) of a K or Q tile, k-step ks
+// (dk 32 ks + 8 g .. + 7): one 16-byte read.
+template <int DK> __device__ inline bf16x8 row_frag(const uint4 *tile, int mt, int ks, int lane) {
+    const int r = 16 * mt + (lane & 15), g = lane >> 4;
+    return __builtin_bit_cast(bf16x8, tile[r * (DK / 8) + xpiece<DK>(r, 4 * ks + g)]);
+}
+
+// A-operand fragment of K^T for state tile t (rows state_row(16 t + i)) and
+// k-step ks over the chunk rows (perm_row order: runs of 4 rows at 32 ks + 4 g
+// and 32 ks + 16 + 4 g): two transposed 8-byte reads.  In each 16-lane group
+// source lane s reads 4 consecutive dk columns of row base + s / 4 and lane
+// 4 c + q receives column (that of source lanes c, c + 4, ...) + q of rows
+// base .. base + 3, so reading the 4 columns 32 (t / 2) + 4 (t % 2) + 8 c
+// gives lane 4 c + q exactly state_row(16 t + 4 c + q).
+template <int DK> __device__ inline bf16x8 kt_frag(const uint4 *k, int t, int ks, int lane) {
     typedef short i16x8 __attribute__((ext_vector_type(8)));
     const int g = lane >> 4, s = lane & 15;
-    const auto lo = RowTile<__bf16>::tr4(kn, ld, 32 * ks + 4 * g + (s >> 2), n0, lane);
-    const auto hi = RowTile<__bf16>::tr4(kn, ld, 32 * ks + 16 + 4 * g + (s >> 2), n0, lane);
-    const i16x8 both = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    const int piece = 4 * (t >> 1) + (s & 3), half = 8 * (t & 1);
+    i16x4 h[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int r = 32 * ks + 16 * u + 4 * g + (s >> 2);
+        const char *p = (const char *)k + (r * (DK / 8) + xpiece<DK>(r, piece)) * 16 + half;
+        h[u] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4 *)p);
+    }
+    const i16x8 both = {h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
     return __builtin_bit_cast(bf16x8, both);
 }
 
+// Workgroup barrier that orders LDS operations only: a workgroup release
+// fence would also wait for the helper waves' global loads of the next chunk
+// and the output stores in flight.
+__device__ inline void xbar_lds() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+// Start state of a wave's two column tiles (permuted rows) from a row-major
+// [DK][DV] fp32 state, or zero.
+template <int DK, int DV>
+__device__ inline void load_state_perm(const float *src, int col0, f32x4 (&S)[2][DK / 16]) {
+    const int lane = threadIdx.x & 63, g16 = lane >> 4, c16 = lane & 15;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int t = 0; t < DK / 16; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                S[c][t][i] = src ? src[(size_t)state_row(16 * t + 4 * g16 + i) * DV + col0 + 16 * c + c16] : 0.f;
+}
+
+// Row-major [DK][DV] store of one column tile of the state (permuted rows);
+// voff is the lane's byte offset of dk row 8 g, its column.
+template <int DK, int DV>
+__device__ inline void store_state_perm(float *dst, const f32x4 (&S)[DK / 16], uint32_t voff) {
+    const auto r = make_rsrc(dst, DK * DV * sizeof(float));
+#pragma unroll
+    for (int t = 0; t < DK / 16; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_int(S[t][i]), r, (int)voff,
+                                                  (32 * (t >> 1) + 4 * (t & 1) + i) * DV * (int)sizeof(float), 0);
+}
+
 template <int DK, int DV, int MODE>
-__global__ __launch_bounds__((2 * xscan_cols<DK, DV>())) void gdr_xscan_kernel(ScanArgs a) {
+__global__ __launch_bounds__((xscan_threads<DK, DV>())) void gdr_xscan_kernel(ScanArgs a) {
     using M = MT<__bf16>;
-    using RTl = RowTile<__bf16>;
     typedef __bf16 T;
     constexpr int CW = xscan_cols<DK, DV>();
-    constexpr int NWV = CW / 32;                       // waves
-    constexpr int NTH = 64 * NWV;                      // threads
+    constexpr bool kOut = MODE != kXMap;
+    constexpr int NPAIR = CW / 32;                     // scan waves (and output waves with kOut)
+    constexpr int NTH = xscan_threads<DK, DV>();
     constexpr int RT = DK / 16, FS = DK / 4, KS = DK / 32;
     constexpr int NCOLS = (MODE == kXMap) ? DK + DV : DV;   // column space of the unit
     constexpr int NP = NCOLS / CW;                     // parts per (sequence, head[, segment])
-    constexpr bool kOut = MODE != kXMap;
     static_assert(NP * CW == NCOLS && (MODE != kXMap || DK % CW == 0), "column parts");
-    using Lds = XLds<DK, CW>;
-    constexpr int LDN = Lds::LDN, LDV = Lds::LDV;
+    using Lds = XLds<DK, CW, kOut>;
+    constexpr int KV = Lds::KV;
     __shared__ Lds sm;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g16 = lane >> 4, c16 = lane & 15;
+    const bool scan_wave = w < NPAIR;
+    const int pr = scan_wave ? w : w - NPAIR;          // the wave's pair
     const int H = a.n_heads;
 
     // ---- unit: (sequence, head[, segment], part); the parts of one chain
@@ -140,209 +209,207 @@ __global__ __launch_bounds__((2 * xscan_cols<DK, DV>())) void gdr_xscan_kernel(S
     }
     const int cb = part * CW;                          // first column of the part
     const bool phi = MODE == kXMap && cb < DK;         // a part of Phi (identity start, no values)
-    const int vcol0 = (MODE == kXMap) ? cb - DK : cb;  // first value column of the part (R / state)
+    const int vcol0 = (MODE == kXMap) ? cb - DK : cb;  // first value (state) column of the part
+    const int pcol = vcol0 + 32 * pr;                  // first state column of the wave's pair
 
-    // ---- state: this wave's two column tiles, all DK rows
-    f32x4 S[2][RT];
-    if constexpr (MODE == kXMap) {
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-            for (int t = 0; t < RT; ++t)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    S[c][t][i] = (phi && 16 * t + 4 * g16 + i == cb + 32 * w + 16 * c + c16) ? 1.f : 0.f;
-    } else if (MODE == kXReplay && sg > 0) {
-        const float *src = a.seg.state + (seg_slot * H + h) * DK * DV;
-#pragma unroll
-        for (int c = 0; c < 2; ++c) load_state_c<RT>(src, (vcol0 + 32 * w + 16 * c) / 16, S[c]);
-    } else {
-        const float *src = start_state(a, seq, h, (size_t)DK * DV, part == 0 && w == 0);
-#pragma unroll
-        for (int c = 0; c < 2; ++c) load_state_tile<DK, DV>(src, (vcol0 + 32 * w) / 16 + c, S[c]);
-    }
-    float dprod = 1.f;   // product of the chunk decays (the map's D)
-
-    // P fragments above the diagonal that no P tile writes stay zero
-    if constexpr (kOut) {
-        for (int e = tid; e < 4 * 2 * 64; e += NTH) (&sm.pf[0][0][0])[e] = make_uint4(0, 0, 0, 0);
-    }
-
-    // ---- staging: chunk jj's inputs into registers, then into LDS buffer
-    constexpr int KP = kChunk * DK / 8;                // 16-byte pieces of K (and of Q)
-    constexpr int VP = kChunk * CW / 8;                // pieces of the part's V columns
-    constexpr int XP = kXFrags * 64, GP = kGateBlock / 4;
-    constexpr int NK = (KP + NTH - 1) / NTH, NV = (VP + NTH - 1) / NTH;
-    constexpr int NX = (XP + NTH - 1) / NTH, NG = (GP + NTH - 1) / NTH;
-    static_assert(KP % NTH == 0 && VP % NTH == 0, "staging tiling");
+    // ---- staging of chunk jj's inputs by the helper waves (the output
+    // waves, or in the map loader waves of their own): global loads into
+    // registers (rows past the chunk's end read as zero through the buffer
+    // range), then 16-byte LDS stores.  Helper wave p stages a quarter of K,
+    // Q and the preparation's block, and pair p's 32 value columns.  The scan
+    // waves issue no global loads, so nothing they read from LDS waits on a
+    // load in flight.
+    constexpr int KPW = KV / 64 / NPAIR;                 // 16-byte pieces of K per helper lane
+    constexpr int MPW = (kMiscVec + 64 * NPAIR - 1) / (64 * NPAIR);
+    constexpr int VPW = kChunk * 32 / 8 / 64;            // pieces of a pair's values per lane (4)
+    static_assert(KPW * 64 * NPAIR == KV, "K staging tiling");
     struct Stage {
-        uint4 k[NK], q[kOut ? NK : 1], v[NV], x[NX], gbv[NG];
+        uint4 k[KPW], q[kOut ? KPW : 1], m[MPW], v[VPW];
     };
     const T *qin = (const T *)a.q, *kin = (const T *)a.k, *vin = (const T *)a.v;
     const bool has_v = !phi;
-    auto load = [&](Stage &st, int jj) {
+    auto stage_load = [&](Stage &st, int jj) {
         int lo, hi;
         chunk_range32(jj, len, a.C, a.cps, &lo, &hi);
         const int n = hi - lo;
-        const int64_t t0 = (int64_t)cu0 + lo;
-        const int64_t sh = (base + jj) * H + h;
+        const int64_t row0 = ((int64_t)cu0 + lo) * H + h;
+        const uint32_t rows_k = head_rows_bytes<T>(n, H, DK);
+        const auto rk = make_rsrc(kin + row0 * DK, rows_k);
+        const auto rq = make_rsrc(qin + row0 * DK, rows_k);
 #pragma unroll
-        for (int it = 0; it < NK; ++it) {
-            const int e = tid + NTH * it, r = e / (DK / 8), c = 8 * (e % (DK / 8));
-            const int64_t row = (t0 + min(r, n - 1)) * H + h;
-            st.k[it] = *(const uint4 *)(kin + row * DK + c);
-            if constexpr (kOut) st.q[it] = *(const uint4 *)(qin + row * DK + c);
-            if (r >= n) {
-                st.k[it] = make_uint4(0, 0, 0, 0);
-                if constexpr (kOut) st.q[it] = make_uint4(0, 0, 0, 0);
-            }
+        for (int it = 0; it < KPW; ++it) {
+            const int e = (pr * KPW + it) * 64 + lane, r = e / (DK / 8), p = e % (DK / 8);
+            const uint32_t voff = (uint32_t)(r * H * DK * 2 + 16 * p);
+            st.k[it] = buf_load16(rk, voff, 0u);
+            if constexpr (kOut) st.q[it] = buf_load16(rq, voff, 0u);
         }
+        const auto rm = make_rsrc(a.ws.misc + ((base + jj) * H + h) * kMiscVec, kMiscVec * 16);
 #pragma unroll
-        for (int it = 0; it < NV; ++it) {
-            const int e = tid + NTH * it, r = e / (CW / 8), c = 8 * (e % (CW / 8));
-            st.v[it] = make_uint4(0, 0, 0, 0);
-            if (has_v && r < n) st.v[it] = *(const uint4 *)(vin + ((t0 + r) * H + h) * DV + vcol0 + c);
-        }
-        const uint4 *xs = (const uint4 *)a.ws.xf + sh * XP;
+        for (int it = 0; it < MPW; ++it)
+            st.m[it] = buf_load16(rm, (uint32_t)(((pr * MPW + it) * 64 + lane) * 16), 0u);
+        const uint32_t vbytes =
+            has_v ? (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)((n - 1) * H * DV + 32) * 2)) : 0u;
+        const auto rv = make_rsrc(vin + row0 * DV + pcol, vbytes);
 #pragma unroll
-        for (int it = 0; it < NX; ++it) {
-            const int e = tid + NTH * it;
-            if (e < XP) st.x[it] = xs[e];
-        }
-        const uint4 *gs = (const uint4 *)(a.ws.gb + sh * kGateBlock);
-#pragma unroll
-        for (int it = 0; it < NG; ++it) {
-            const int e = tid + NTH * it;
-            if (e < GP) st.gbv[it] = gs[e];
+        for (int it = 0; it < VPW; ++it) {
+            const int e = it * 64 + lane, r = e >> 2, p = e & 3;
+            st.v[it] = buf_load16(rv, (uint32_t)(r * H * DV * 2 + 16 * p), 0u);
         }
     };
-    auto store = [&](const Stage &st, int bi) {
+    auto stage_store_shared = [&](const Stage &st, int bi) {
         typename Lds::Buf &B = sm.buf[bi];
 #pragma unroll
-        for (int it = 0; it < NK; ++it) {
-            const int e = tid + NTH * it, r = e / (DK / 8), m = e % (DK / 8);
-            *(uint4 *)&B.kn[r][8 * m] = st.k[it];
-            const int p = xperm_pos8(m);
-            *(uint2 *)&B.kp[r][p] = make_uint2(st.k[it].x, st.k[it].y);
-            *(uint2 *)&B.kp[r][p + 8] = make_uint2(st.k[it].z, st.k[it].w);
-            if constexpr (kOut) {
-                *(uint2 *)&B.qp[r][p] = make_uint2(st.q[it].x, st.q[it].y);
-                *(uint2 *)&B.qp[r][p + 8] = make_uint2(st.q[it].z, st.q[it].w);
-            }
+        for (int it = 0; it < KPW; ++it) {
+            const int e = (pr * KPW + it) * 64 + lane, r = e / (DK / 8), p = e % (DK / 8);
+            B.k[r * (DK / 8) + xpiece<DK>(r, p)] = st.k[it];
+            if constexpr (kOut) B.q[r * (DK / 8) + xpiece<DK>(r, p)] = st.q[it];
         }
 #pragma unroll
-        for (int it = 0; it < NV; ++it) {
-            const int e = tid + NTH * it, r = e / (CW / 8), c = 8 * (e % (CW / 8));
-            *(uint4 *)&B.v[r][c] = st.v[it];
-        }
-#pragma unroll
-        for (int it = 0; it < NX; ++it) {
-            const int e = tid + NTH * it;
-            if (e < XP) (&B.xf[0][0])[e] = st.x[it];
-        }
-#pragma unroll
-        for (int it = 0; it < NG; ++it) {
-            const int e = tid + NTH * it;
-            if (e < GP) ((uint4 *)B.gb)[e] = st.gbv[it];
+        for (int it = 0; it < MPW; ++it) {
+            const int e = (pr * MPW + it) * 64 + lane;
+            if (e < kMiscVec) B.misc[e] = st.m[it];
         }
     };
-
-    // ---- checkpoints (single-level scan only)
-    CkptDst ck;
-    if constexpr (MODE == kXScan) ck.init(a, seq, h, len, (size_t)DK * DV, part == 0 && w == 0);
-    uint32_t lane_off[2];
+    auto stage_store_values = [&](const Stage &st) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) lane_off[c] = 4u * (uint32_t)(4 * g16 * DV + vcol0 + 32 * w + 16 * c + c16);
+        for (int it = 0; it < VPW; ++it) sm.v[pr][it * 64 + lane] = st.v[it];
+    };
 
-    const float scale = a.scale;
-    Stage st;
-    load(st, c0);
-    store(st, 0);
-    __syncthreads();
+    // P fragments above the diagonal that no P tile writes stay zero
+    if constexpr (kOut) {
+        for (int e = tid; e < 4 * 2 * 64; e += NTH) sm.pf[e] = make_uint4(0, 0, 0, 0);
+    }
 
-    for (int jj = c0; jj < c1; ++jj) {
-        const int bi = (jj - c0) & 1;
-        const typename Lds::Buf &B = sm.buf[bi];
-        if (jj + 1 < c1) load(st, jj + 1);
-        int lo, hi;
-        chunk_range32(jj, len, a.C, a.cps, &lo, &hi);
-        const int n = hi - lo;
+    if (scan_wave) {
+        // ================================ scan wave ================================
+        f32x4 S[2][RT];
+        if constexpr (MODE == kXMap) {
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int t = 0; t < RT; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        S[c][t][i] = (phi && state_row(16 * t + 4 * g16 + i) == cb + 32 * pr + 16 * c + c16) ? 1.f : 0.f;
+        } else if (MODE == kXReplay && sg > 0) {
+            const float *src = a.seg.state + (seg_slot * H + h) * DK * DV;
+#pragma unroll
+            for (int c = 0; c < 2; ++c) load_state_c<RT>(src, pcol / 16 + c, S[c]);
+        } else {
+            load_state_perm<DK, DV>(start_state(a, seq, h, (size_t)DK * DV, part == 0 && pr == 0), pcol, S);
+        }
+        float dprod = 1.f;   // product of the chunk decays (the map's D)
+        CkptDst ck;
+        if constexpr (MODE == kXScan) ck.init(a, seq, h, len, (size_t)DK * DV, part == 0 && pr == 0);
+        uint32_t soff[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) soff[c] = 4u * (uint32_t)(8 * g16 * DV + pcol + 16 * c + c16);
 
-        // S_0 as B operand (and A operand of S_0^T), dk permuted by perm_row
+        // S_0 as bf16 B operand (k-step ks: dk 32 ks + 8 g .. + 7)
         T sb[2][FS];
+        auto make_sb = [&]() {
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
+            for (int c = 0; c < 2; ++c)
 #pragma unroll
-            for (int f = 0; f < FS; ++f) sb[c][f] = (T)S[c][f >> 2][f & 3];
-
-        // ---- Y = K S_0, O^T = S_0^T Q^T, and this wave's P tiles, by row tile
-        f32x4 Y[2][4], O[2][4];
-        typename M::frag kf[4][KS];
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) kf[mt][ks] = M::pack(&B.kp[16 * mt + c16][32 * ks + 8 * g16]);
-#pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                Y[c][mt] = zero4();
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) Y[c][mt] = M::mma(kf[mt][ks], M::pack(&sb[c][8 * ks]), Y[c][mt]);
-            }
+                for (int f = 0; f < FS; ++f) sb[c][f] = (T)S[c][f >> 2][f & 3];
             if constexpr (kOut) {
-                typename M::frag qf[KS];
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) qf[ks] = M::pack(&B.qp[16 * mt + c16][32 * ks + 8 * g16]);
+                for (int c = 0; c < 2; ++c)
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) sm.sbh[pr][c][ks][lane] = *(const uint4 *)&sb[c][8 * ks];
+            }
+        };
+        make_sb();
+        xbar_lds();
+
+        for (int jj = c0; jj < c1; ++jj) {
+            const int bi = (jj - c0) & 1;
+            const typename Lds::Buf &B = sm.buf[bi];
+            int lo, hi;
+            chunk_range32(jj, len, a.C, a.cps, &lo, &hi);
+            // the page id of a checkpoint this chunk ends on
+            int ckid = 0;
+            if constexpr (MODE == kXScan) {
+                if (hi % a.C == 0) ckid = ck.load_id(hi / a.C - 1);
+            }
+
+            // Each phase issues its LDS reads ahead of the MFMAs that use them
+            // (sched_barrier keeps the order): one wave per SIMD pair half
+            // cannot hide LDS latency otherwise.
+            // ---- Y = K S_0: row tiles 0-1's K fragments in flight, then 2-3's
+            // behind the first half of the MFMAs
+            bf16x8 kf[4][KS];
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) kf[mt][ks] = row_frag<DK>(B.k, mt, ks, lane);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int mt = 2; mt < 4; ++mt)
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) kf[mt][ks] = row_frag<DK>(B.k, mt, ks, lane);
+            f32x4 Y[2][4];
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
                 for (int c = 0; c < 2; ++c) {
-                    O[c][mt] = zero4();
+                    Y[c][mt] = zero4();
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) O[c][mt] = M::mma(M::pack(&sb[c][8 * ks]), qf[ks], O[c][mt]);
+                    for (int ks = 0; ks < KS; ++ks) Y[c][mt] = M::mma(kf[mt][ks], M::pack(&sb[c][8 * ks]), Y[c][mt]);
                 }
-                // P tiles (mt, nt), nt <= mt: tile index mt (mt + 1) / 2 + nt,
-                // dealt to the waves round-robin
+            __builtin_amdgcn_sched_barrier(0);
+            // the reads of Z and U (values, gates, X) behind the second half of Y
+            const float *gate = (const float *)&B.misc[kXFrags * 64];
+            float4 d4[4], b4[4];
+            i16x4 vr[2][4];
 #pragma unroll
-                for (int nt = 0; nt <= mt; ++nt) {
-                    if ((mt * (mt + 1) / 2 + nt) % NWV != w) continue;   // wave-uniform
-                    f32x4 p = zero4();
+            for (int mt = 0; mt < 4; ++mt) {
+                d4[mt] = *(const float4 *)&gate[kChunk + 16 * mt + 4 * g16];
+                b4[mt] = *(const float4 *)&gate[2 * kChunk + 16 * mt + 4 * g16];
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) p = M::mma(kf[nt][ks], qf[ks], p);
-                    // lane (g, c): P[r = 16 mt + c][s = 16 nt + 4 g + i]
-                    const float gr = B.gb[16 * mt + c16] * kLog2e;
-                    const float4 gs = *(const float4 *)&B.gb[16 * nt + 4 * g16];
-                    const float gsv[4] = {gs.x, gs.y, gs.z, gs.w};
-                    T pv[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int s = 16 * nt + 4 * g16 + i, r = 16 * mt + c16;
-                        pv[i] = (T)(s <= r ? p[i] * __builtin_amdgcn_exp2f(gr - gsv[i] * kLog2e) : 0.f);
-                    }
-                    *(uint2 *)((char *)&sm.pf[mt][nt >> 1][lane] + 8 * (nt & 1)) = *(const uint2 *)pv;
-                }
+                for (int c = 0; c < 2; ++c)
+                    vr[c][mt] = RowTile<T>::tr4((const T *)&sm.v[pr][0], 32, 16 * mt + 4 * g16 + ((lane & 15) >> 2), 16 * c, lane);
             }
-        }
-
-        // ---- Z = diag(beta) V - diag(d) Y, then U = X Z
-        f32x4 U[2][4];
-        {
+            bf16x8 xf[kXFrags];
+#pragma unroll
+            for (int e = 0; e < kXFrags; ++e) xf[e] = __builtin_bit_cast(bf16x8, B.misc[e * 64 + lane]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int mt = 2; mt < 4; ++mt)
+#pragma unroll
+                for (int c = 0; c < 2; ++c) {
+                    Y[c][mt] = zero4();
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) Y[c][mt] = M::mma(kf[mt][ks], M::pack(&sb[c][8 * ks]), Y[c][mt]);
+                }
+            __builtin_amdgcn_sched_barrier(0);
+            // the K^T fragments of the state update's first half, in flight behind Z
+            bf16x8 kt[RT][2];
+#pragma unroll
+            for (int t = 0; t < RT / 2; ++t)
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) kt[t][ks] = kt_frag<DK>(B.k, t, ks, lane);
+            __builtin_amdgcn_sched_barrier(0);
+            // ---- Z = diag(beta) V - diag(d) Y; U = X Z
             T zb[2][16];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
-                const float4 d4 = *(const float4 *)&B.gb[kChunk + 16 * mt + 4 * g16];
-                const float4 b4 = *(const float4 *)&B.gb[2 * kChunk + 16 * mt + 4 * g16];
-                const float dv[4] = {d4.x, d4.y, d4.z, d4.w}, bv[4] = {b4.x, b4.y, b4.z, b4.w};
+                const float dv[4] = {d4[mt].x, d4[mt].y, d4[mt].z, d4[mt].w};
+                const float bv[4] = {b4[mt].x, b4[mt].y, b4[mt].z, b4[mt].w};
 #pragma unroll
-                for (int c = 0; c < 2; ++c) {
-                    float vv[4] = {0.f, 0.f, 0.f, 0.f};
-                    if (has_v) {
-                        float o4[4];
-                        RTl::col4(&B.v[0][0], LDV, mt, 32 * w + 16 * c, lane, o4);
+                for (int c = 0; c < 2; ++c)
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) vv[i] = o4[i];
-                    }
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) zb[c][4 * mt + i] = (T)(bv[i] * vv[i] - dv[i] * Y[c][mt][i]);
-                }
+                    for (int i = 0; i < 4; ++i)
+                        zb[c][4 * mt + i] = (T)(bv[i] * (float)__builtin_bit_cast(T, (short)vr[c][mt][i]) - dv[i] * Y[c][mt][i]);
             }
+            __builtin_amdgcn_sched_barrier(0);
+            // the second half's K^T fragments, in flight behind U
+#pragma unroll
+            for (int t = RT / 2; t < RT; ++t)
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) kt[t][ks] = kt_frag<DK>(B.k, t, ks, lane);
+            __builtin_amdgcn_sched_barrier(0);
+            f32x4 U[2][4];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
@@ -350,112 +417,323 @@ __global__ __launch_bounds__((2 * xscan_cols<DK, DV>())) void gdr_xscan_kernel(S
                     U[c][mt] = zero4();
 #pragma unroll
                     for (int ks = 0; ks <= (mt >> 1); ++ks)
-                        U[c][mt] = M::mma(M::pack((const T *)&B.xf[xfrag_slot(mt, ks)][lane]), M::pack(&zb[c][8 * ks]),
-                                          U[c][mt]);
+                        U[c][mt] = M::mma(xf[xfrag_slot(mt, ks)], M::pack(&zb[c][8 * ks]), U[c][mt]);
                 }
-        }
-
-        // ---- state update: S = exp(G_63) S + K^T diag(exp(G_63 - G)) U
-        T ub[2][16], ub2[2][16];
+            // ---- U to the output wave (unscaled), and diag(exp(G_63 - G)) U
+            T ub2[2][16];
+            {
+                float4 e4[4];
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            const float4 e4 = *(const float4 *)&B.gb[3 * kChunk + 16 * mt + 4 * g16];
-            const float ev[4] = {e4.x, e4.y, e4.z, e4.w};
+                for (int mt = 0; mt < 4; ++mt) e4[mt] = *(const float4 *)&gate[3 * kChunk + 16 * mt + 4 * g16];
+                T ub[2][16];
 #pragma unroll
-            for (int c = 0; c < 2; ++c)
+                for (int mt = 0; mt < 4; ++mt) {
+                    const float ev[4] = {e4[mt].x, e4[mt].y, e4[mt].z, e4[mt].w};
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    ub[c][4 * mt + i] = (T)U[c][mt][i];
-                    ub2[c][4 * mt + i] = (T)(U[c][mt][i] * ev[i]);
+                    for (int c = 0; c < 2; ++c)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            ub[c][4 * mt + i] = (T)U[c][mt][i];
+                            ub2[c][4 * mt + i] = (T)(U[c][mt][i] * ev[i]);
+                        }
                 }
-        }
-        const float eL = __builtin_amdgcn_exp2f(B.gb[kChunk - 1] * kLog2e);
-        dprod *= eL;
+                if constexpr (kOut) {
 #pragma unroll
-        for (int t = 0; t < RT; ++t) {
-            typename M::frag kt[2];
+                    for (int c = 0; c < 2; ++c)
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) kt[ks] = kt_frag(&B.kn[0][0], LDN, ks, 16 * t, lane);
-#pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                f32x4 acc = S[c][t] * eL;
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) acc = M::mma(kt[ks], M::pack(&ub2[c][8 * ks]), acc);
-                S[c][t] = acc;
+                        for (int ks = 0; ks < 2; ++ks) sm.ubh[pr][c][ks][lane] = *(const uint4 *)&ub[c][8 * ks];
+                }
+                xbar_lds();   // B_jj: U handed off (the output waves' P tiles are written); the
+                              // values of chunk jj are read, so the helpers may replace them
             }
-        }
-        if constexpr (MODE == kXScan) {
-            // checkpoint when the chunk ends on a multiple of C (positions are
-            // local and start on a multiple of C)
-            if (hi % a.C == 0) {
-                if (float *d = ck.next(ck.load_id(hi / a.C - 1))) {
+            // ---- S = exp(G_63) S + K^T diag(exp(G_63 - G)) U
+            const float eL = __builtin_amdgcn_exp2f(gate[kChunk - 1] * kLog2e);
+            dprod *= eL;
 #pragma unroll
-                    for (int c = 0; c < 2; ++c) store_state_tiles<RT, DV>(d, S[c], lane_off[c]);
-                }
-            }
-        }
-
-        if constexpr (kOut) {
-            lds_barrier();   // every wave's P tiles are in LDS
-            // ---- O^T = scale ((S_0^T Q^T) diag(exp G) + U^T P^T), stored 4 columns per lane
-            T *obase = (T *)a.o + (((int64_t)cu0 + lo) * H + h) * DV;
-            const auto ro = make_rsrc(obase, head_rows_bytes<T>(n, H, DV));
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                const float eg = __builtin_amdgcn_exp2f(B.gb[16 * mt + c16] * kLog2e);
+            for (int t = 0; t < RT; ++t)
 #pragma unroll
                 for (int c = 0; c < 2; ++c) {
-                    f32x4 acc = O[c][mt] * eg;
+                    f32x4 acc = S[c][t] * eL;
 #pragma unroll
-                    for (int ks = 0; ks <= (mt >> 1); ++ks)
-                        acc = M::mma(M::pack(&ub[c][8 * ks]), M::pack((const T *)&sm.pf[mt][ks][lane]), acc);
-                    T out[4];
+                    for (int ks = 0; ks < 2; ++ks) acc = M::mma(kt[t][ks], M::pack(&ub2[c][8 * ks]), acc);
+                    S[c][t] = acc;
+                }
+            if constexpr (MODE == kXScan) {
+                // checkpoint when the chunk ends on a multiple of C (positions are
+                // local and start on a multiple of C)
+                if (hi % a.C == 0) {
+                    if (float *d = ck.next(ckid)) {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) out[i] = (T)(acc[i] * scale);
-                    const uint32_t voff = ((uint32_t)(16 * mt + c16) * (uint32_t)(H * DV) +
-                                           (uint32_t)(vcol0 + 32 * w + 16 * c + 4 * g16)) * (uint32_t)sizeof(T);
-                    buf_store8(*(const uint2 *)out, ro, voff, 0u);
+                        for (int c = 0; c < 2; ++c) store_state_perm<DK, DV>(d, S[c], soff[c]);
+                    }
                 }
             }
+            make_sb();
+            xbar_lds();   // C_jj: chunk jj + 1's inputs and the state handoff are in LDS
         }
-        // chunk jj + 1's inputs into the other buffer; every wave has
-        // finished reading it (chunk jj - 1) before the last barrier
-        if (jj + 1 < c1) store(st, bi ^ 1);
-        lds_barrier();
-    }
 
-    // ---- epilogue
-    if constexpr (MODE == kXScan) {
-        if (a.final_state) {
+        // ---- epilogue
+        if constexpr (MODE == kXScan) {
+            if (a.final_state) {
 #pragma unroll
-            for (int c = 0; c < 2; ++c)
-                store_state_tiles<RT, DV>(a.final_state + (size_t)pair * DK * DV, S[c], lane_off[c]);
-        }
-    }
-    if constexpr (MODE == kXMap) {
-        const int64_t ssh = seg_slot * H + h;
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            const int col = cb + 32 * w + 16 * c + c16;
-            if (phi) {
-                T *dst = (T *)a.seg.phi + ssh * DK * DK + phi_col_pos(col);
-#pragma unroll
-                for (int t = 0; t < RT; ++t)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int r = 16 * t + 4 * g16 + e;
-                        dst[(size_t)r * DK] = (T)(S[c][t][e] - (r == col ? dprod : 0.f));
-                    }
-            } else {
-                float4 *dst = (float4 *)(a.seg.r + ssh * DK * DV);
-                const int tile = (col - DK) / 16;
-#pragma unroll
-                for (int t = 0; t < RT; ++t)
-                    dst[(tile * RT + t) * 64 + lane] = make_float4(S[c][t][0], S[c][t][1], S[c][t][2], S[c][t][3]);
+                for (int c = 0; c < 2; ++c)
+                    store_state_perm<DK, DV>(a.final_state + (size_t)pair * DK * DV, S[c], soff[c]);
             }
         }
-        if (part == 0 && w == 0 && lane == 0) a.seg.d[ssh] = dprod;
+        if constexpr (MODE == kXMap) {
+            const int64_t ssh = seg_slot * H + h;
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const int col = cb + 32 * pr + 16 * c + c16;
+                if (phi) {
+                    // Phi' = Phi - D I, row-major [DK][DK] in the io type
+                    T *dst = (T *)a.seg.phi + ssh * DK * DK + col;
+#pragma unroll
+                    for (int t = 0; t < RT; ++t)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int r = state_row(16 * t + 4 * g16 + e);
+                            dst[(size_t)r * DK] = (T)(S[c][t][e] - (r == col ? dprod : 0.f));
+                        }
+                } else {
+                    float4 *dst = (float4 *)(a.seg.r + ssh * DK * DV);
+                    const int tile = (col - DK) / 16;
+#pragma unroll
+                    for (int t = 0; t < RT; ++t)
+                        dst[(tile * RT + t) * 64 + lane] = make_float4(S[c][t][0], S[c][t][1], S[c][t][2], S[c][t][3]);
+                }
+            }
+            if (part == 0 && pr == 0 && lane == 0) a.seg.d[ssh] = dprod;
+        }
+    } else {
+        // ============================ helper (output) wave ============================
+        // Stages every chunk's inputs one chunk ahead and, with an output,
+        // reads the output out.
+        Stage st;
+        stage_load(st, c0);
+        stage_store_shared(st, 0);
+        stage_store_values(st);
+        xbar_lds();
+        [[maybe_unused]] const float scale = a.scale;
+        for (int jj = c0; jj < c1; ++jj) {
+            const int bi = (jj - c0) & 1;
+            const typename Lds::Buf &B = sm.buf[bi];
+            int lo, hi;
+            chunk_range32(jj, len, a.C, a.cps, &lo, &hi);
+            [[maybe_unused]] const int n = hi - lo;
+            [[maybe_unused]] const float *gate = (const float *)&B.misc[kXFrags * 64];
+            if (jj + 1 < c1) stage_load(st, jj + 1);
+            [[maybe_unused]] f32x4 O[2][4];   // S_0^T Q^T, finished after B_jj
+            if constexpr (kOut) {
+                // S_0 handed over at the end of the previous chunk, the Q fragments
+                // and the K fragments of this wave's P tiles, all in flight first.
+                // P tiles (mt, nt), nt <= mt: tile index mt (mt + 1) / 2 + nt,
+                // dealt to the output waves round-robin.
+                bf16x8 sb[2][KS], qf[4][KS];
+#pragma unroll
+                for (int c = 0; c < 2; ++c)
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) sb[c][ks] = __builtin_bit_cast(bf16x8, sm.sbh[pr][c][ks][lane]);
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) qf[mt][ks] = row_frag<DK>(B.q, mt, ks, lane);
+                // K fragments of this wave's P tiles: column block nt = pr (and
+                // nt = 0 for the tile (3, 0) the last wave takes over)
+                bf16x8 pk[KS], pk0[KS];
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) pk[ks] = row_frag<DK>(B.k, pr, ks, lane);
+                if (pr == NPAIR - 1 && NPAIR > 1) {
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) pk0[ks] = row_frag<DK>(B.k, 0, ks, lane);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                // ---- S_0^T Q^T
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                    for (int c = 0; c < 2; ++c) {
+                        O[c][mt] = zero4();
+#pragma unroll
+                        for (int ks = 0; ks < KS; ++ks) O[c][mt] = M::mma(sb[c][ks], qf[mt][ks], O[c][mt]);
+                    }
+                // ---- P tiles (mt, nt), nt <= mt, lane (g, c) holding
+                // P[r = 16 mt + c][s = 16 nt + 4 g + i]: wave p takes the tiles of
+                // column block p (with NPAIR = 4 the tile (3, 0) moves from wave 0
+                // to wave 3, which balances them 3, 3, 2, 2); with two waves, wave
+                // 1 also takes column blocks 2 and 3.
+                auto p_tile = [&](int mt, int nt, const bf16x8 (&kk)[KS], const bf16x8 (&qq)[KS]) {
+                    f32x4 p = zero4();
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) p = M::mma(kk[ks], qq[ks], p);
+                    const float gr = gate[16 * mt + c16] * kLog2e;
+                    const float4 gs = *(const float4 *)&gate[16 * nt + 4 * g16];
+                    const float gsv[4] = {gs.x, gs.y, gs.z, gs.w};
+                    T pv[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int s_ = 16 * nt + 4 * g16 + e, r = 16 * mt + c16;
+                        pv[e] = (T)(s_ <= r ? p[e] * __builtin_amdgcn_exp2f(gr - gsv[e] * kLog2e) : 0.f);
+                    }
+                    *(uint2 *)((char *)&sm.pf[(2 * mt + (nt >> 1)) * 64 + lane] + 8 * (nt & 1)) = *(const uint2 *)pv;
+                };
+                if constexpr (NPAIR == 4) {
+#pragma unroll
+                    for (int mt = 0; mt < 4; ++mt) {
+                        if (mt >= pr && !(pr == 0 && mt == 3)) p_tile(mt, pr, pk, qf[mt]);   // wave-uniform
+                    }
+                    if (pr == 3) p_tile(3, 0, pk0, qf[3]);
+                } else {
+                    // two waves: wave 0 column block 0 (4 tiles), wave 1 blocks 1..3 (6 tiles)
+#pragma unroll
+                    for (int mt = 0; mt < 4; ++mt) {
+                        if (pr == 0) p_tile(mt, 0, pk, qf[mt]);
+#pragma unroll
+                        for (int nt = 1; nt <= mt; ++nt) {
+                            if (pr == 1) {
+                                bf16x8 kk[KS];
+#pragma unroll
+                                for (int ks = 0; ks < KS; ++ks) kk[ks] = row_frag<DK>(B.k, nt, ks, lane);
+                                p_tile(mt, nt, kk, qf[mt]);
+                            }
+                        }
+                    }
+                }
+            }
+            xbar_lds();   // B_jj
+            if constexpr (kOut) {
+                // ---- O^T = scale ((S_0^T Q^T) diag(exp G) + U^T P^T), 4 columns per lane
+                bf16x8 ubf[2][2], pfr[kXFrags];
+#pragma unroll
+                for (int c = 0; c < 2; ++c)
+#pragma unroll
+                    for (int ks = 0; ks < 2; ++ks) ubf[c][ks] = __builtin_bit_cast(bf16x8, sm.ubh[pr][c][ks][lane]);
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                    for (int ks = 0; ks <= (mt >> 1); ++ks)
+                        pfr[xfrag_slot(mt, ks)] = __builtin_bit_cast(bf16x8, sm.pf[(2 * mt + ks) * 64 + lane]);
+                float eg[4];
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) eg[mt] = __builtin_amdgcn_exp2f(gate[16 * mt + c16] * kLog2e);
+                __builtin_amdgcn_sched_barrier(0);
+                T *obase = (T *)a.o + (((int64_t)cu0 + lo) * H + h) * DV;
+                const auto ro = make_rsrc(obase, head_rows_bytes<T>(n, H, DV));
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                    for (int c = 0; c < 2; ++c) {
+                        f32x4 acc = O[c][mt] * eg[mt];
+#pragma unroll
+                        for (int ks = 0; ks <= (mt >> 1); ++ks) acc = M::mma(ubf[c][ks], pfr[xfrag_slot(mt, ks)], acc);
+                        T out[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) out[e] = (T)(acc[e] * scale);
+                        const uint32_t voff = ((uint32_t)(16 * mt + c16) * (uint32_t)(H * DV) +
+                                               (uint32_t)(pcol + 16 * c + 4 * g16)) * (uint32_t)sizeof(T);
+                        buf_store8(*(const uint2 *)out, ro, voff, 0u);
+                    }
+            }
+            // chunk jj + 1's inputs: the other buffer was last read in chunk
+            // jj - 1, and the scan wave has read chunk jj's values (B_jj)
+            if (jj + 1 < c1) {
+                stage_store_shared(st, bi ^ 1);
+                stage_store_values(st);
+            }
+            xbar_lds();   // C_jj
+        }
     }
+}
+
+// Two-level scan, second level: per (sequence, head, 16-column tile), the
+// segment states in order, S <- D S + Phi' S + R (the large D I part stays
+// in fp32; only Phi' S goes through the bf16 MFMA).  The state's rows are
+// held in the fused scan's permutation (state_row), as are R and the
+// segment-entering states it exchanges with the map and the replay; Phi' is
+// row-major [DK][DK].  Writes the checkpoints (segment ends on a multiple of
+// C), the state entering every later segment, and the final state.
+template <int DK, int DV>
+__global__ __launch_bounds__(64) void gdr_xcombine_kernel(ScanArgs a) {
+    using M = MT<__bf16>;
+    typedef __bf16 T;
+    constexpr int RT = DK / 16, NT = DV / 16, FS = DK / 4, KS = DK / 32;
+    constexpr int kMfmas = RT * KS, kLoads = 1 + RT + RT * KS;
+    const int lane = threadIdx.x, g16 = lane >> 4, c16 = lane & 15;
+    const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
+    const int pair = chain_of_rank(a, xcd + 8 * (q / NT)), tile = q % NT;
+    const int H = a.n_heads;
+    if (pair < 0) return;
+    const int seq = pair / H, h = pair % H;
+    const int cu0 = a.cu[seq], len = a.cu[seq + 1] - cu0;
+    const int nch = n_chunks32(len, a.C, a.cps);
+    const int nseg = (nch + a.seg_m - 1) / a.seg_m;
+    const int64_t sbase = slot_base_dev(cu0, seq, (int64_t)a.C * a.seg_m, a.cps);
+    const int col = 16 * tile + c16;
+    f32x4 S[RT];
+    {
+        const float *src = start_state(a, seq, h, (size_t)DK * DV, tile == 0);
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) S[t][i] = src ? src[(size_t)state_row(16 * t + 4 * g16 + i) * DV + col] : 0.f;
+    }
+    CkptDst ck;
+    ck.init(a, seq, h, len, (size_t)DK * DV, tile == 0);
+    const uint32_t soff = 4u * (uint32_t)(8 * g16 * DV + col);
+    __builtin_amdgcn_s_waitcnt(0);
+
+    struct Ops {
+        float d;
+        int ckid;             // page id of the checkpoint this segment would end (paged)
+        f32x4 r[RT];
+        uint4 ph[RT][KS];
+    };
+    auto load = [&](Ops &o, int sg) {
+        const int64_t ssh = (sbase + sg) * H + h;
+        o.ckid = ck.load_id(max((sg + 1) * a.seg_m / a.cps - 1, 0));
+        o.d = buf_load4f(make_rsrc(a.seg.d + ssh, sizeof(float)), 0u, 0u);
+        const auto rr = make_rsrc(a.seg.r + ssh * DK * DV, DK * DV * sizeof(float));
+#pragma unroll
+        for (int t = 0; t < RT; ++t) {
+            const uint4 x = buf_load16(rr, 16u * lane, 1024u * (tile * RT + t));
+            o.r[t] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
+        }
+        // A operand of Phi' for state tile t: row state_row(16 t + c), dk 32 ks + 8 g .. + 7
+        const auto rp = make_rsrc((const T *)a.seg.phi + ssh * DK * DK, DK * DK * sizeof(T));
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                o.ph[t][ks] = buf_load16(rp, (uint32_t)((state_row(16 * t + c16) * DK + 8 * g16) * sizeof(T)),
+                                         (uint32_t)(32 * ks * sizeof(T)));
+    };
+    auto step = [&](const Ops &o, int sg) {
+        T sb[FS];
+#pragma unroll
+        for (int f = 0; f < FS; ++f) sb[f] = (T)S[f >> 2][f & 3];
+#pragma unroll
+        for (int t = 0; t < RT; ++t) {
+            f32x4 acc = S[t] * o.d + o.r[t];
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                acc = M::mma(__builtin_bit_cast(bf16x8, o.ph[t][ks]), M::pack(&sb[8 * ks]), acc);
+            S[t] = acc;
+        }
+#pragma unroll
+        for (int i = 0; i < kMfmas; ++i) {
+            if (i < kLoads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+        if (kLoads > kMfmas) __builtin_amdgcn_sched_group_barrier(0x020, kLoads - kMfmas, 0);
+        int lo, hi;
+        chunk_range32(min((sg + 1) * a.seg_m, nch) - 1, len, a.C, a.cps, &lo, &hi);
+        if (sg + 1 < nseg) store_state_c<RT>(a.seg.state + ((sbase + sg + 1) * H + h) * DK * DV, tile, S);
+        if (hi % a.C == 0) {   // checkpoints come in order, one per C-aligned segment end
+            if (float *d = ck.next(o.ckid)) store_state_perm<DK, DV>(d, S, soff);
+        }
+    };
+    scan_ring<1>(nseg, load, step, (Ops *)nullptr);
+    if (a.final_state) store_state_perm<DK, DV>(a.final_state + (size_t)pair * DK * DV, S, soff);
 }
 
 }  // namespace la

@@ -257,8 +257,7 @@ __host__ inline int64_t chunk_grid_blocks(int n_seqs, int n_heads, int64_t max_c
 struct Workspace {
     void *w, *kt, *sc, *u, *p, *qf, *ut;
     float *g;
-    void *xf;          // fused path: X fragments per slot-head
-    float *gb;         // fused path: gate blocks per slot-head
+    uint4 *misc;       // fused path: per slot-head, the X fragments and the gate block
 };
 
 // U~ tile vector `vec` (= column tile * 4 + row tile) of one slot-head, as

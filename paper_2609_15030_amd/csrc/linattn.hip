@@ -99,13 +99,13 @@ la_status check_shape(const la_shape *s) {
 }
 
 // Workspace regions (byte offsets; 0 = absent).  Per chunk slot and head:
-//   bf16: X fragments (6 KB) and the gate block (1 KB);
+//   bf16: the X fragments (6 KB) and the gate block (1 KB), in one block;
 //   fp32: -W, K~^T, U~, G, P and Q in operand order, plus the state entering
 //         each chunk and U for the output kernel of the dk-split scan.
 // The two-level scan adds, per segment slot and head, Phi' (io type), R, D
 // and the state entering the segment.
 struct WsPlan {
-    size_t xf, gb;                           // bf16 forms
+    size_t misc;                             // bf16 forms
     size_t w, kt, ut, g, sc, u, pm, qf;      // fp32 forms
     size_t phi, segr, segd, segst;           // two-level scan (seg_m >= 2)
     int seg_m;
@@ -122,8 +122,7 @@ WsPlan plan_workspace(const la_shape *s, int64_t total_tokens) {
     size_t off = kRegionAlign;   // offset 0 marks an absent region
     auto take = [&](size_t bytes) { const size_t at = off; off = round_up(off + bytes, kRegionAlign); return at; };
     if (s->io_dtype == LA_BF16) {
-        p.xf = take(sh * la::kXFrags * 64 * 16);
-        p.gb = take(sh * la::kGateBlock * sizeof(float));
+        p.misc = take(sh * la::kMiscVec * 16);
     } else {
         p.w = take(sh * la::kChunk * s->dk * io);
         p.kt = take(sh * s->dk * la::kChunk * io);
@@ -231,13 +230,12 @@ la_status launch_fused(const PrefillCall &c, const WsPlan &p, int64_t max_chunks
     const int cps = la::chunks_per_interval(s->ckpt_interval);
     char *base = (char *)c.workspace;
     la::Workspace ws{};
-    ws.xf = base + p.xf;
-    ws.gb = (float *)(base + p.gb);
+    ws.misc = (uint4 *)(base + p.misc);
     trace_mark(0, c.stream);
     (void)hipGetLastError();
     if (max_chunks > 0) {
         la::XPrepArgs pa{c.k, c.g, c.beta, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps, s->variant,
-                         (int32_t)max_chunks, ws.xf, ws.gb,
+                         (int32_t)max_chunks, ws.misc,
                          la::chunk_major_map(s->n_seqs, s->n_heads, max_chunks) ? 1 : 0};
         const int64_t blocks = la::chunk_grid_blocks(s->n_seqs, s->n_heads, max_chunks);
         hipLaunchKernelGGL((la::gdr_xprep_kernel<DK>), dim3((unsigned)blocks), dim3(256), 0, c.stream, pa);
@@ -258,20 +256,20 @@ la_status launch_fused(const PrefillCall &c, const WsPlan &p, int64_t max_chunks
         const int64_t units = pairs * sa.max_seg;
         if (units > 0) {
             hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, la::kXMap>), dim3((unsigned)(8 * NPM * ((units + 7) / 8))),
-                               dim3(2 * CW), 0, c.stream, sa);
+                               dim3(la::xscan_threads<DK, DV>()), 0, c.stream, sa);
             if (la_status e = hip_check("segment map launch")) return e;
         }
-        hipLaunchKernelGGL((la::gdr_seg_combine_kernel<__bf16, DK, DV>), dim3((unsigned)(8 * (DV / 16) * ((pairs + 7) / 8))),
+        hipLaunchKernelGGL((la::gdr_xcombine_kernel<DK, DV>), dim3((unsigned)(8 * (DV / 16) * ((pairs + 7) / 8))),
                            dim3(64), 0, c.stream, sa);
         if (la_status e = hip_check("segment combine launch")) return e;
         if (units > 0) {
             hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, la::kXReplay>), dim3((unsigned)(8 * NP * ((units + 7) / 8))),
-                               dim3(2 * CW), 0, c.stream, sa);
+                               dim3(la::xscan_threads<DK, DV>()), 0, c.stream, sa);
             if (la_status e = hip_check("segment replay launch")) return e;
         }
     } else {
         hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, la::kXScan>), dim3((unsigned)(8 * NP * ((pairs + 7) / 8))),
-                           dim3(2 * CW), 0, c.stream, sa);
+                           dim3(la::xscan_threads<DK, DV>()), 0, c.stream, sa);
         if (la_status e = hip_check("fused scan launch")) return e;
     }
     trace_mark(2, c.stream);
