@@ -387,11 +387,14 @@ const char *la_last_error_message(void);
 
 /*
  * la_trace_set_events - profiling hook.  When `events` holds at least 4
- * hipEvent_t (created by the caller), every later la_prefill /
- * la_prefill_resume call on this thread records events[0] before its first
- * kernel, events[1] after the chunk-preparation kernel, events[2] after the
- * inter-chunk scan kernel and events[3] after the output kernel, all on the
- * call's stream.  n_events = 0 (or events = NULL) switches it off.
+ * hipEvent_t (created by the caller), every later la_prefill,
+ * la_prefill_resume and la_prefill_paged call on this thread records, on the
+ * call's stream, events[0] before its first kernel, events[1] after the
+ * chunk-preparation kernel, events[2] after the segment maps and their
+ * combine (two-level forms; directly after events[1] otherwise) and
+ * events[3] after the last scan kernel (the fused scan, the segment replay,
+ * or the fp32 scan and output kernels).  The events are overwritten by each
+ * call.  n_events = 0 (or events = NULL) switches it off.
  */
 void la_trace_set_events(void *const *events, int32_t n_events);
 

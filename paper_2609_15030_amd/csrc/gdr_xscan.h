@@ -59,11 +59,12 @@ enum : int { kXScan = 0, kXReplay = 1, kXMap = 2 };
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
-// Columns per workgroup: a whole 128-column head on four wave pairs; 64
-// columns on two when a head dimension is 64 (the map's Phi and R parts then
-// split at a part boundary).
-template <int DK, int DV> constexpr int xscan_cols() { return (DK == 128 && DV == 128) ? 128 : 64; }
-template <int DK, int DV> constexpr int xscan_threads() { return 64 * (xscan_cols<DK, DV>() / 32) * 2; }
+// Columns per workgroup (CW): 128 (four wave pairs) or 64 (two).  Every
+// column's arithmetic is the same whatever CW, so the choice is free: 64
+// spreads a chain over more CUs when there are few chains, 128 stages each
+// chunk's K, Q and prepared block once for twice the columns.  The map's Phi
+// and R parts split at a part boundary, so CW divides dk.
+constexpr int xscan_threads(int cw) { return 64 * (cw / 32) * 2; }
 
 // dk row held at state tile-row x = 16 t + 4 g + q (lane group g, element
 // q of tile t): the B-operand contraction index 8 ks + j of lane group g
@@ -159,14 +160,14 @@ __device__ inline void store_state_perm(float *dst, const f32x4 (&S)[DK / 16], u
                                                   (32 * (t >> 1) + 4 * (t & 1) + i) * DV * (int)sizeof(float), 0);
 }
 
-template <int DK, int DV, int MODE>
-__global__ __launch_bounds__((xscan_threads<DK, DV>())) void gdr_xscan_kernel(ScanArgs a) {
+template <int DK, int DV, int MODE, int CW>
+__global__ __launch_bounds__((xscan_threads(CW))) void gdr_xscan_kernel(ScanArgs a) {
     using M = MT<__bf16>;
     typedef __bf16 T;
-    constexpr int CW = xscan_cols<DK, DV>();
+    static_assert(CW == 64 || CW == 128, "column width");
     constexpr bool kOut = MODE != kXMap;
     constexpr int NPAIR = CW / 32;                     // scan waves (and output waves with kOut)
-    constexpr int NTH = xscan_threads<DK, DV>();
+    constexpr int NTH = xscan_threads(CW);
     constexpr int RT = DK / 16, FS = DK / 4, KS = DK / 32;
     constexpr int NCOLS = (MODE == kXMap) ? DK + DV : DV;   // column space of the unit
     constexpr int NP = NCOLS / CW;                     // parts per (sequence, head[, segment])

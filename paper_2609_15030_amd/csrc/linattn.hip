@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -43,6 +44,7 @@ la_status hip_check(const char *what) {
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
 constexpr size_t kRegionAlign = 256;
+constexpr int64_t kDeviceCUs = 256;   // compute units of an MI355X (gfx950)
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -165,7 +167,9 @@ struct PrefillCall {
 };
 
 // Profiling hook (la_trace_set_events): events recorded on the launch stream
-// at the start, after the preparation, after the scan and at the end.
+// at the start, after the preparation, after the segment maps and combine
+// (two-level forms only; at the same point as the previous event otherwise)
+// and at the end.
 void trace_mark(int i, hipStream_t stream) {
     if (g_trace_n >= 4) (void)hipEventRecord((hipEvent_t)g_trace[i], stream);
 }
@@ -222,6 +226,26 @@ la::ScanArgs scan_args(const PrefillCall &c, const la::Workspace &ws) {
     return sa;
 }
 
+// The fused scan kernel of one mode over `units` independent units, at the
+// column width that still gives every CU two workgroups (128 columns), else
+// at 64 columns, which spreads each unit over more CUs.  The width never
+// changes a result: every column's arithmetic is the same at both.
+template <int DK, int DV, int MODE>
+la_status launch_xscan(const la::ScanArgs &sa, int64_t units, hipStream_t stream, const char *what) {
+    constexpr int NCOLS = MODE == la::kXMap ? DK + DV : DV;
+    auto go = [&](auto width) {
+        constexpr int CW = decltype(width)::value;
+        const int64_t blocks = 8 * (NCOLS / CW) * ((units + 7) / 8);
+        hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, MODE, CW>), dim3((unsigned)blocks),
+                           dim3(la::xscan_threads(CW)), 0, stream, sa);
+        return hip_check(what);
+    };
+    if constexpr (DK == 128 && DV == 128) {
+        if (units * (NCOLS / 128) >= 2 * kDeviceCUs) return go(std::integral_constant<int, 128>{});
+    }
+    return go(std::integral_constant<int, 64>{});
+}
+
 // bf16: preparation, then the fused scan, or the two-level scan (segment
 // maps, combine, fused replay).
 template <int DK, int DV>
@@ -243,8 +267,6 @@ la_status launch_fused(const PrefillCall &c, const WsPlan &p, int64_t max_chunks
     }
     trace_mark(1, c.stream);
     la::ScanArgs sa = scan_args(c, ws);
-    constexpr int CW = la::xscan_cols<DK, DV>();
-    constexpr int NP = DV / CW, NPM = (DK + DV) / CW;
     const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
     if (p.seg_m > 1) {
         sa.seg_m = p.seg_m;
@@ -254,25 +276,19 @@ la_status launch_fused(const PrefillCall &c, const WsPlan &p, int64_t max_chunks
         sa.seg.d = (float *)(base + p.segd);
         sa.seg.state = (float *)(base + p.segst);
         const int64_t units = pairs * sa.max_seg;
-        if (units > 0) {
-            hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, la::kXMap>), dim3((unsigned)(8 * NPM * ((units + 7) / 8))),
-                               dim3(la::xscan_threads<DK, DV>()), 0, c.stream, sa);
-            if (la_status e = hip_check("segment map launch")) return e;
-        }
+        if (units > 0)
+            if (la_status e = launch_xscan<DK, DV, la::kXMap>(sa, units, c.stream, "segment map launch")) return e;
         hipLaunchKernelGGL((la::gdr_xcombine_kernel<DK, DV>), dim3((unsigned)(8 * (DV / 16) * ((pairs + 7) / 8))),
                            dim3(64), 0, c.stream, sa);
         if (la_status e = hip_check("segment combine launch")) return e;
-        if (units > 0) {
-            hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, la::kXReplay>), dim3((unsigned)(8 * NP * ((units + 7) / 8))),
-                               dim3(la::xscan_threads<DK, DV>()), 0, c.stream, sa);
-            if (la_status e = hip_check("segment replay launch")) return e;
-        }
+        trace_mark(2, c.stream);
+        if (units > 0)
+            if (la_status e = launch_xscan<DK, DV, la::kXReplay>(sa, units, c.stream, "segment replay launch"))
+                return e;
     } else {
-        hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, la::kXScan>), dim3((unsigned)(8 * NP * ((pairs + 7) / 8))),
-                           dim3(la::xscan_threads<DK, DV>()), 0, c.stream, sa);
-        if (la_status e = hip_check("fused scan launch")) return e;
+        trace_mark(2, c.stream);
+        if (la_status e = launch_xscan<DK, DV, la::kXScan>(sa, pairs, c.stream, "fused scan launch")) return e;
     }
-    trace_mark(2, c.stream);
     trace_mark(3, c.stream);
     return LA_OK;
 }
@@ -311,14 +327,14 @@ la_status launch_f32(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) 
     const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
     if (prefill_form(s) == LA_FORM_TILE_SCAN_OUT) {
         // the scan's output wave produces the output: no output launch
+        trace_mark(2, c.stream);
         hipLaunchKernelGGL((la::gdr_scan1o_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(128), 0, c.stream, sa);
         if (la_status e = hip_check("inter-chunk scan launch")) return e;
-        trace_mark(2, c.stream);
     } else {
+        trace_mark(2, c.stream);
         hipLaunchKernelGGL((la::gdr_scan_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(64 * la::ScanGeom<DK>::NW), 0,
                            c.stream, sa);
         if (la_status e = hip_check("inter-chunk scan launch")) return e;
-        trace_mark(2, c.stream);
         if (max_chunks > 0) {
             la::OutArgs oa{c.o, c.cu_dev, s->n_seqs, s->n_heads, s->ckpt_interval, cps, (int32_t)max_chunks, s->scale,
                            ws, chunk_major};

@@ -273,3 +273,26 @@ def test_two_level_head_dims(dk, dv):
     torch.cuda.synchronize()
     s = int(x.cu_seqlens[i])
     assert torch.equal(r2.o, res.o[s + B:s + lens[i]]) and torch.equal(r2.final_state[0], res.final_state[i])
+
+
+def test_column_width_does_not_change_bits():
+    """64 sequences x 8 heads (512 chains: the fused scan runs 128-column
+    workgroups) against one of them alone (8 chains: 64-column workgroups):
+    parity with the oracle on every head, and the lone sequence's output,
+    checkpoints and final state equal its rows in the batch bit for bit."""
+    rng = np.random.default_rng(640)
+    lens = [int(n) for n in rng.integers(1, 300, size=64)]
+    H, C = 8, 128
+    x = wl.random_inputs(640, lens, H, 128, 128, wl.BF16)
+    xd, res = _run_cold(x, C)
+    ref = oracle_run(x, interval=C)
+    compare(res, ref, x.cu_seqlens, TOL[la.LA_BF16], "64 seqs x 8 heads, 128-column workgroups")
+    cu = x.cu_seqlens
+    for i in (int(np.argmax(lens)), 5):
+        alone = api.prefill(api.to_device(x.seq(i)), C)
+        torch.cuda.synchronize()
+        s, e = int(cu[i]), int(cu[i + 1])
+        off = int(res.ckpt_offsets[i])
+        assert torch.equal(alone.o, res.o[s:e]) and torch.equal(alone.final_state[0], res.final_state[i])
+        if alone.n_ckpt_rows:
+            assert torch.equal(alone.ckpt, res.ckpt[off:off + alone.n_ckpt_rows])
