@@ -241,6 +241,29 @@ la_status la_prefill_paged(const la_shape *shape, const la_pages *pages,
                            void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * la_prefill_paged_noalloc - la_prefill_paged without a workspace argument,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).  The call
+ * allocates nothing: its workspace is a 64 MiB static device array inside
+ * the library, one per device, held until the process ends (its address is
+ * looked up once per device, on the first call there).  Calls whose
+ * workspace (la_prefill_workspace_bytes for the shape and cu_seqlens[n_seqs]
+ * tokens) exceeds 64 MiB return LA_ERR_WORKSPACE before any launch.  Every
+ * call on a device shares that device's array, and nothing in it has to
+ * start at zero (each call writes what it reads); calls that overlap on one
+ * device (e.g. on two streams) race and must not be issued.  Arguments,
+ * results and other errors as la_prefill_paged.
+ */
+la_status la_prefill_paged_noalloc(const la_shape *shape, const la_pages *pages,
+                                   const void *q, const void *k, const void *v,
+                                   const float *g, const float *beta,
+                                   const int32_t *cu_seqlens_dev, const int32_t *cu_seqlens_host,
+                                   const int64_t *start_pos_dev, const int64_t *start_pos_host,
+                                   void *o, float *final_state,
+                                   const int32_t *ckpt_offsets_dev, const int32_t *ckpt_offsets_host,
+                                   void *stream);
+
+/*
  * la_decode_step - decode continuation: advance every (sequence, head) by one
  * generated token from its fp32 state (the recurrent state of section 2.1,
  * continued after a cold prefill or a reload; sections 5.1, 5.4 and 5.5

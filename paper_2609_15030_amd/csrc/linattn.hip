@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 #include <cmath>
 #include <cstdarg>
@@ -20,6 +21,13 @@
 #include "gdr_decode.h"
 #include "paged.h"
 #include "hybrid.h"
+
+// Workspace of la_prefill_paged_noalloc, for callers that cannot allocate:
+// a file-scope device array, one copy per device the library runs on, held
+// until the process ends.  Host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace {
 
@@ -42,6 +50,30 @@ la_status hip_check(const char *what) {
 }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Device address of `scratch` on the current device: looked up once per
+// device (with that device current), then reused.  std::call_once makes the
+// lookup race-free; the table is written only inside it.
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void *g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+la_status scratch_address(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return fail(LA_ERR_HIP, "no current device for the static scratch (device %d)", dev);
+    std::call_once(g_scratch_once[dev], [dev]() {
+        void *ptr = nullptr;
+        g_scratch_err[dev] = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        g_scratch_ptr[dev] = ptr;
+    });
+    if (g_scratch_err[dev] != hipSuccess || !g_scratch_ptr[dev])
+        return fail(LA_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                    hipGetErrorString(g_scratch_err[dev]));
+    *out = g_scratch_ptr[dev];
+    return LA_OK;
+}
 
 constexpr size_t kRegionAlign = 256;
 constexpr int64_t kDeviceCUs = 256;   // compute units of an MI355X (gfx950)
@@ -724,6 +756,26 @@ la_status la_prefill_paged(const la_shape *shape, const la_pages *pages, const v
                   nullptr, o, final_state, nullptr, ckpt_offsets_dev, ckpt_offsets_host, workspace, ws_bytes,
                   (hipStream_t)stream, pages};
     return run_prefill(c);
+}
+
+la_status la_prefill_paged_noalloc(const la_shape *shape, const la_pages *pages, const void *q, const void *k,
+                                   const void *v, const float *g, const float *beta, const int32_t *cu_seqlens_dev,
+                                   const int32_t *cu_seqlens_host, const int64_t *start_pos_dev,
+                                   const int64_t *start_pos_host, void *o, float *final_state,
+                                   const int32_t *ckpt_offsets_dev, const int32_t *ckpt_offsets_host, void *stream) {
+    if (la_status e = check_shape(shape)) return e;
+    if (!cu_seqlens_host) return fail(LA_ERR_INVALID_ARG, "cu_seqlens_host is required");
+    const int64_t total = cu_seqlens_host[shape->n_seqs];
+    if (total < 0) return fail(LA_ERR_INVALID_ARG, "cu_seqlens[n_seqs]=%lld", (long long)total);
+    const size_t need = plan_workspace(shape, total).total;
+    if (need > kScratchBytes)
+        return fail(LA_ERR_WORKSPACE, "the call needs %zu bytes of workspace; the static scratch holds %zu", need,
+                    kScratchBytes);
+    void *ws = nullptr;
+    if (la_status e = scratch_address(&ws)) return e;
+    return la_prefill_paged(shape, pages, q, k, v, g, beta, cu_seqlens_dev, cu_seqlens_host, start_pos_dev,
+                            start_pos_host, o, final_state, ckpt_offsets_dev, ckpt_offsets_host, ws, kScratchBytes,
+                            stream);
 }
 
 la_status la_decode_step(const la_shape *shape, const void *q, const void *k, const void *v, const float *g,

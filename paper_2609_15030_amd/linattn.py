@@ -32,7 +32,7 @@ LA_GDR_LITERAL = 0
 LA_GDR_DECAYED_DELTA = 1
 
 EXPORTED = ("strict_prefix_boundary", "la_prefill_workspace_bytes", "la_prefill",
-            "la_prefill_resume", "la_checkpoint_rows", "la_prefill_form", "la_prefill_paged", "la_decode_step", "la_state_save_paged",
+            "la_prefill_resume", "la_checkpoint_rows", "la_prefill_form", "la_prefill_paged", "la_prefill_paged_noalloc", "la_decode_step", "la_state_save_paged",
             "la_state_restore_paged",
             "la_state_save_host", "la_state_restore_host", "la_hybrid_boundary", "la_hybrid_restore",
             "la_status_string", "la_last_error_message", "la_trace_set_events")
@@ -90,6 +90,7 @@ def _load() -> ctypes.CDLL:
         "la_checkpoint_rows": ([I32, P, P, I64, P, ctypes.POINTER(I64)], I32),
         "la_prefill_form": ([SH], I32),
         "la_prefill_paged": ([SH, ctypes.POINTER(LaPages), P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
+        "la_prefill_paged_noalloc": ([SH, ctypes.POINTER(LaPages), P, P, P, P, P, P, P, P, P, P, P, P, P, P], I32),
         "la_decode_step": ([SH, P, P, P, P, P, P, P, P], I32),
         "la_state_save_paged": ([P, I64, I64, P, I64, P, P, P], I32),
         "la_state_restore_paged": ([P, I64, P, P, I64, I64, P, P], I32),
@@ -277,6 +278,23 @@ def la_prefill_paged(shape: LaShape, pages: Optional[LaPages], q, k, v, g, beta,
                                _dptr(start_dev), _hptr(sh, np.int64), _dptr(o), _dptr(final_state),
                                _dptr(ckpt_off_dev), _hptr(oh, np.int32), _dptr(workspace),
                                workspace.numel() * workspace.element_size(), _stream(stream))
+    if check:
+        _check(st)
+    return st
+
+
+def la_prefill_paged_noalloc(shape: LaShape, pages: Optional[LaPages], q, k, v, g, beta, cu_dev, cu_host, start_dev,
+                             start_host, o, final_state, ckpt_off_dev, ckpt_off_host, stream=None,
+                             check: bool = True) -> int:
+    """la_prefill_paged on the library's static workspace (no allocation)."""
+    cu_host = np.ascontiguousarray(cu_host, dtype=np.int32)
+    sh = None if start_host is None else np.ascontiguousarray(start_host, dtype=np.int64)
+    oh = None if ckpt_off_host is None else np.ascontiguousarray(ckpt_off_host, dtype=np.int32)
+    st = _lib.la_prefill_paged_noalloc(ctypes.byref(shape), None if pages is None else ctypes.byref(pages),
+                                       _dptr(q), _dptr(k), _dptr(v), _dptr(g), _dptr(beta), _dptr(cu_dev),
+                                       _hptr(cu_host, np.int32), _dptr(start_dev), _hptr(sh, np.int64), _dptr(o),
+                                       _dptr(final_state), _dptr(ckpt_off_dev), _hptr(oh, np.int32),
+                                       _stream(stream))
     if check:
         _check(st)
     return st
