@@ -23,9 +23,9 @@ writes equals what the cold run wrote (a resume reproduces the recompute
 bit for bit), so repeated steps see the same pool.
 
 Timing: per-step intervals from HIP events on the launch stream.  Before
-each timed step a 512 MiB buffer is written to flush the MALL (the last
-level cache); ``value`` and ``ms_per_step`` come from the median of those
-cold-cache steps, with min, mean and a back-to-back warm-cache figure beside
+each timed step a 512 MiB buffer is written and another 512 MiB read, which
+flushes the MALL (the last level cache) and leaves it clean; ``value`` and
+``ms_per_step`` come from the median of those cold-cache steps, with min, mean and a back-to-back warm-cache figure beside
 them.  Per-kernel durations come from events the library records inside the
 call (la_trace_set_events).  Prefill tokens/s counts the tokens each call
 computes (sum of n_i - B_i).
@@ -152,14 +152,21 @@ class Timer:
         self.torch = torch
         self.sp = stream_ptr
         self.buf = torch.empty(MALL_FLUSH_BYTES, dtype=torch.uint8, device="cuda")
+        self.clean = torch.ones(MALL_FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
         self.k = 0
 
     def flush(self):
+        """Write 512 MiB, then read another 512 MiB: the last-level cache then
+        holds none of the timed work's data and no dirty lines whose
+        write-back the timed work would pay for."""
         self.k = (self.k + 1) & 0xFF
         self.buf.fill_(self.k)
+        self.clean.sum()
 
     def cold(self, run, reps):
-        """Per-repetition ms, the MALL flushed before each repetition."""
+        """Per-repetition ms, the MALL flushed before each repetition; the GPU
+        time from the first repetition's start to the last one's end (flushes
+        included) is kept in ``last_span_ms``."""
         ev = HipEvents(2 * reps)
         self.torch.cuda.synchronize()
         self.torch.cuda._sleep(20_000_000)
@@ -168,19 +175,20 @@ class Timer:
             ev.record(2 * r, self.sp)
             run()
             ev.record(2 * r + 1, self.sp)
+        self.last_span_ms = ev.ms(0, 2 * reps - 1)
         return [ev.ms(2 * r, 2 * r + 1) for r in range(reps)]
 
     def warm(self, run, reps):
-        """Mean ms over back-to-back repetitions."""
-        ev = HipEvents(2)
+        """Per-repetition ms over back-to-back repetitions (no flush)."""
+        ev = HipEvents(2 * reps)
         self.torch.cuda.synchronize()
         self.torch.cuda._sleep(20_000_000)
         run()
-        ev.record(0, self.sp)
-        for _ in range(reps):
+        for r in range(reps):
+            ev.record(2 * r, self.sp)
             run()
-        ev.record(1, self.sp)
-        return ev.ms(0, 1) / reps
+            ev.record(2 * r + 1, self.sp)
+        return [ev.ms(2 * r, 2 * r + 1) for r in range(reps)]
 
     def stages(self, la, run, reps):
         """Mean per-stage ms from the library's trace events (cold cache):
@@ -386,7 +394,7 @@ def bench_tp_rank(api, la, torch, wl, timer, reps):
     torch.cuda.synchronize()
     assert torch.equal(both.o[N:], both.o[B:N]) and torch.equal(both.final[1], both.final[0])
     ms = timer.cold(step, reps)
-    warm = timer.warm(step, reps)
+    warm = statistics.median(timer.warm(step, reps))
     stg = timer.stages(la, step, max(3, reps // 2))
     T = N + (N - B)
     return {"workload": w.name, "form": la.la_prefill_form(both.shape), "tokens_per_step": T,
@@ -523,11 +531,9 @@ def headline(args, torch, api, la, wl, timer, sp):
     v.check(torch)
     # the timed region: K steps, each after a MALL flush
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
     ms = timer.cold(v.run_step, args.steps)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    res = {"v": v, "ms": ms, "wall": wall}
+    res = {"v": v, "ms": ms, "span": timer.last_span_ms}
     if args.only_headline:
         n = 4096
         perm = torch.from_numpy(np.random.default_rng(7).permutation(n).astype(np.int32)).cuda()
@@ -725,14 +731,14 @@ def main():
                    "ckpt_interval": v.C, "pool_pages": v.w.pool_pages,
                    "modes": {m: v.w.modes.count(m) for m in ("cold", "complete", "partial")}},
         "timing": {"value_from": "median of the K per-step HIP-event intervals, MALL flushed before each",
-                   **summary(ms), "wall_ms_per_step_incl_flush": round(h["wall"] * 1e3 / args.steps, 4)},
+                   **summary(ms), "gpu_ms_per_step_incl_flush": round(h["span"] / args.steps, 4)},
     }
     if args.only_headline:
         print(json.dumps(out), flush=True)
         return
     st = h["stages"]
     fl = flops_per_token_head(dk, dv)
-    out["timing"]["warm_us"] = round(h["warm"] * 1e3, 2)
+    out["timing"]["warm"] = summary(h["warm"])
     out["step_call"] = {"form": la.la_prefill_form(v.step_call.shape),
                         "stage_us": {k: round(x * 1e3, 2) for k, x in st.items()},
                         "alg_tflops": round(sum(fl.values()) * T * H / med / 1e12, 3),
