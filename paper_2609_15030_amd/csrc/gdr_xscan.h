@@ -57,6 +57,12 @@ namespace la {
 
 enum : int { kXScan = 0, kXReplay = 1, kXMap = 2 };
 
+// Waves per workgroup: a scan wave and a helper per 32-column pair.  The
+// 64-column form with an output gives each pair a third wave: one helper
+// then reads the output out and the other (the loader) stages the inputs.
+constexpr bool xscan_loaders(int cw, int mode) { return cw == 64 && mode != kXMap; }
+constexpr int xscan_threads(int cw, int mode) { return 64 * (cw / 32) * (xscan_loaders(cw, mode) ? 3 : 2); }
+
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 // Columns per workgroup (CW): 128 (four wave pairs) or 64 (two).  Every
@@ -64,7 +70,6 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 // spreads a chain over more CUs when there are few chains, 128 stages each
 // chunk's K, Q and prepared block once for twice the columns.  The map's Phi
 // and R parts split at a part boundary, so CW divides dk.
-constexpr int xscan_threads(int cw) { return 64 * (cw / 32) * 2; }
 
 // dk row held at state tile-row x = 16 t + 4 g + q (lane group g, element
 // q of tile t): the B-operand contraction index 8 ks + j of lane group g
@@ -75,7 +80,7 @@ __device__ __host__ inline int state_row(int x) {
     return 32 * (t >> 1) + 8 * g + 4 * (t & 1) + q;
 }
 
-template <int DK, int CW, bool OUT> struct XLds {
+template <int DK, int CW, bool OUT, int NVB> struct XLds {
     static constexpr int NPAIR = CW / 32;
     static constexpr int KV = kChunk * DK / 8;   // 16-byte pieces of a chunk's K (or Q)
     struct Buf {
@@ -84,7 +89,8 @@ template <int DK, int CW, bool OUT> struct XLds {
         uint4 misc[kMiscVec];                    // X fragments, then the gate block
     };
     Buf buf[2];
-    uint4 v[NPAIR][kChunk * 32 / 8];             // each pair's 32 value columns, row-major [64][32]
+    uint4 v[NVB][NPAIR][kChunk * 32 / 8];        // each pair's 32 value columns, row-major [64][32]
+                                                 // (double-buffered when loader waves stage them)
     uint4 pf[OUT ? 4 * 2 * 64 : 1];              // P fragments [row tile][k-step][lane]
     uint4 sbh[OUT ? NPAIR : 1][2][DK / 32][64];  // S_0 handed to the output wave (B-operand fragments)
     uint4 ubh[OUT ? NPAIR : 1][2][2][64];        // U handed to the output wave
@@ -161,26 +167,29 @@ __device__ inline void store_state_perm(float *dst, const f32x4 (&S)[DK / 16], u
 }
 
 template <int DK, int DV, int MODE, int CW>
-__global__ __launch_bounds__((xscan_threads(CW))) void gdr_xscan_kernel(ScanArgs a) {
+__global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(ScanArgs a) {
     using M = MT<__bf16>;
     typedef __bf16 T;
     static_assert(CW == 64 || CW == 128, "column width");
     constexpr bool kOut = MODE != kXMap;
     constexpr int NPAIR = CW / 32;                     // scan waves (and output waves with kOut)
-    constexpr int NTH = xscan_threads(CW);
+    constexpr int NTH = xscan_threads(CW, MODE);
+    constexpr bool kLoad3 = xscan_loaders(CW, MODE);   // loader waves of their own
     constexpr int RT = DK / 16, FS = DK / 4, KS = DK / 32;
     constexpr int NCOLS = (MODE == kXMap) ? DK + DV : DV;   // column space of the unit
     constexpr int NP = NCOLS / CW;                     // parts per (sequence, head[, segment])
     static_assert(NP * CW == NCOLS && (MODE != kXMap || DK % CW == 0), "column parts");
-    using Lds = XLds<DK, CW, kOut>;
+    constexpr int NVB = kLoad3 ? 2 : 1;                // value buffers
+    using Lds = XLds<DK, CW, kOut, NVB>;
     constexpr int KV = Lds::KV;
     __shared__ Lds sm;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g16 = lane >> 4, c16 = lane & 15;
-    const bool scan_wave = w < NPAIR;
-    const int pr = scan_wave ? w : w - NPAIR;          // the wave's pair
+    const int role = w / NPAIR;                        // 0 scan, 1 helper, 2 loader (kLoad3)
+    const bool scan_wave = role == 0;
+    const int pr = w % NPAIR;                          // the wave's pair
     const int H = a.n_heads;
 
     // ---- unit: (sequence, head[, segment], part); the parts of one chain
@@ -271,9 +280,9 @@ __global__ __launch_bounds__((xscan_threads(CW))) void gdr_xscan_kernel(ScanArgs
             if (e < kMiscVec) B.misc[e] = st.m[it];
         }
     };
-    auto stage_store_values = [&](const Stage &st) {
+    auto stage_store_values = [&](const Stage &st, int bi) {
 #pragma unroll
-        for (int it = 0; it < VPW; ++it) sm.v[pr][it * 64 + lane] = st.v[it];
+        for (int it = 0; it < VPW; ++it) sm.v[bi % NVB][pr][it * 64 + lane] = st.v[it];
     };
 
     // P fragments above the diagonal that no P tile writes stay zero
@@ -369,7 +378,7 @@ __global__ __launch_bounds__((xscan_threads(CW))) void gdr_xscan_kernel(ScanArgs
                 b4[mt] = *(const float4 *)&gate[2 * kChunk + 16 * mt + 4 * g16];
 #pragma unroll
                 for (int c = 0; c < 2; ++c)
-                    vr[c][mt] = RowTile<T>::tr4((const T *)&sm.v[pr][0], 32, 16 * mt + 4 * g16 + ((lane & 15) >> 2), 16 * c, lane);
+                    vr[c][mt] = RowTile<T>::tr4((const T *)&sm.v[bi % NVB][pr][0], 32, 16 * mt + 4 * g16 + ((lane & 15) >> 2), 16 * c, lane);
             }
             bf16x8 xf[kXFrags];
 #pragma unroll
@@ -506,14 +515,39 @@ __global__ __launch_bounds__((xscan_threads(CW))) void gdr_xscan_kernel(ScanArgs
             }
             if (part == 0 && pr == 0 && lane == 0) a.seg.d[ssh] = dprod;
         }
+    } else if (role == 2) {
+        // ================================ loader wave ================================
+        // (kLoad3) Stages chunk jj + 1's inputs at the start of chunk jj, from
+        // registers loaded during chunk jj - 1, then loads chunk jj + 2's.
+        // The buffers written were last read in chunk jj - 1.
+        if constexpr (kLoad3) {
+            Stage st;
+            stage_load(st, c0);
+            stage_store_shared(st, 0);
+            stage_store_values(st, 0);
+            if (c0 + 1 < c1) stage_load(st, c0 + 1);
+            xbar_lds();
+            for (int jj = c0; jj < c1; ++jj) {
+                const int bi = (jj - c0) & 1;
+                if (jj + 1 < c1) {
+                    stage_store_shared(st, bi ^ 1);
+                    stage_store_values(st, bi ^ 1);
+                }
+                if (jj + 2 < c1) stage_load(st, jj + 2);
+                xbar_lds();   // B_jj
+                xbar_lds();   // C_jj
+            }
+        }
     } else {
         // ============================ helper (output) wave ============================
-        // Stages every chunk's inputs one chunk ahead and, with an output,
-        // reads the output out.
-        Stage st;
-        stage_load(st, c0);
-        stage_store_shared(st, 0);
-        stage_store_values(st);
+        // Reads the output out and, without loader waves, stages every
+        // chunk's inputs one chunk ahead.
+        [[maybe_unused]] Stage st;
+        if constexpr (!kLoad3) {
+            stage_load(st, c0);
+            stage_store_shared(st, 0);
+            stage_store_values(st, 0);
+        }
         xbar_lds();
         [[maybe_unused]] const float scale = a.scale;
         for (int jj = c0; jj < c1; ++jj) {
@@ -523,7 +557,9 @@ __global__ __launch_bounds__((xscan_threads(CW))) void gdr_xscan_kernel(ScanArgs
             chunk_range32(jj, len, a.C, a.cps, &lo, &hi);
             [[maybe_unused]] const int n = hi - lo;
             [[maybe_unused]] const float *gate = (const float *)&B.misc[kXFrags * 64];
-            if (jj + 1 < c1) stage_load(st, jj + 1);
+            if constexpr (!kLoad3) {
+                if (jj + 1 < c1) stage_load(st, jj + 1);
+            }
             [[maybe_unused]] f32x4 O[2][4];   // S_0^T Q^T, finished after B_jj
             if constexpr (kOut) {
                 // S_0 handed over at the end of the previous chunk, the Q fragments
@@ -561,8 +597,8 @@ __global__ __launch_bounds__((xscan_threads(CW))) void gdr_xscan_kernel(ScanArgs
                 // ---- P tiles (mt, nt), nt <= mt, lane (g, c) holding
                 // P[r = 16 mt + c][s = 16 nt + 4 g + i]: wave p takes the tiles of
                 // column block p (with NPAIR = 4 the tile (3, 0) moves from wave 0
-                // to wave 3, which balances them 3, 3, 2, 2); with two waves, wave
-                // 1 also takes column blocks 2 and 3.
+                // to wave 3, which balances them 3, 3, 2, 2); with two waves, five
+                // tiles each.
                 auto p_tile = [&](int mt, int nt, const bf16x8 (&kk)[KS], const bf16x8 (&qq)[KS]) {
                     f32x4 p = zero4();
 #pragma unroll
@@ -585,18 +621,25 @@ __global__ __launch_bounds__((xscan_threads(CW))) void gdr_xscan_kernel(ScanArgs
                     }
                     if (pr == 3) p_tile(3, 0, pk0, qf[3]);
                 } else {
-                    // two waves: wave 0 column block 0 (4 tiles), wave 1 blocks 1..3 (6 tiles)
+                    // two waves, five tiles each: wave 0 column block 0 and the
+                    // tile (1, 1), wave 1 the rest of column blocks 1..3
+                    if (pr == 0) {
 #pragma unroll
-                    for (int mt = 0; mt < 4; ++mt) {
-                        if (pr == 0) p_tile(mt, 0, pk, qf[mt]);
+                        for (int mt = 0; mt < 4; ++mt) p_tile(mt, 0, pk, qf[mt]);
+                        bf16x8 kk[KS];
 #pragma unroll
-                        for (int nt = 1; nt <= mt; ++nt) {
-                            if (pr == 1) {
-                                bf16x8 kk[KS];
+                        for (int ks = 0; ks < KS; ++ks) kk[ks] = row_frag<DK>(B.k, 1, ks, lane);
+                        p_tile(1, 1, kk, qf[1]);
+                    } else {
 #pragma unroll
-                                for (int ks = 0; ks < KS; ++ks) kk[ks] = row_frag<DK>(B.k, nt, ks, lane);
-                                p_tile(mt, nt, kk, qf[mt]);
-                            }
+                        for (int mt = 2; mt < 4; ++mt) p_tile(mt, 1, pk, qf[mt]);
+#pragma unroll
+                        for (int nt = 2; nt < 4; ++nt) {
+                            bf16x8 kk[KS];
+#pragma unroll
+                            for (int ks = 0; ks < KS; ++ks) kk[ks] = row_frag<DK>(B.k, nt, ks, lane);
+#pragma unroll
+                            for (int mt = nt; mt < 4; ++mt) p_tile(mt, nt, kk, qf[mt]);
                         }
                     }
                 }
@@ -635,11 +678,13 @@ __global__ __launch_bounds__((xscan_threads(CW))) void gdr_xscan_kernel(ScanArgs
                         buf_store8(*(const uint2 *)out, ro, voff, 0u);
                     }
             }
-            // chunk jj + 1's inputs: the other buffer was last read in chunk
-            // jj - 1, and the scan wave has read chunk jj's values (B_jj)
-            if (jj + 1 < c1) {
-                stage_store_shared(st, bi ^ 1);
-                stage_store_values(st);
+            // chunk jj + 1's inputs: the other buffers were last read in chunk
+            // jj - 1
+            if constexpr (!kLoad3) {
+                if (jj + 1 < c1) {
+                    stage_store_shared(st, bi ^ 1);
+                    stage_store_values(st, bi ^ 1);
+                }
             }
             xbar_lds();   // C_jj
         }

@@ -269,7 +269,7 @@ la_status launch_xscan(const la::ScanArgs &sa, int64_t units, hipStream_t stream
         constexpr int CW = decltype(width)::value;
         const int64_t blocks = 8 * (NCOLS / CW) * ((units + 7) / 8);
         hipLaunchKernelGGL((la::gdr_xscan_kernel<DK, DV, MODE, CW>), dim3((unsigned)blocks),
-                           dim3(la::xscan_threads(CW)), 0, stream, sa);
+                           dim3(la::xscan_threads(CW, MODE)), 0, stream, sa);
         return hip_check(what);
     };
     if constexpr (DK == 128 && DV == 128) {
