@@ -143,7 +143,24 @@ struct CkptDst {
     __device__ int load_id(int r) const {
         return __builtin_amdgcn_raw_buffer_load_b32(ids, (int)((uint32_t)r * (uint32_t)H * 4u), 0, 0);
     }
-    // Destination of the next checkpoint; id is load_id() of its row.
+    // Page ids of local rows [win, win + 64) in the lanes (lane l: row
+    // win + l), read once per 64 rows: a read per checkpoint would put a wait
+    // for every store in flight before the next one.
+    int idv = 0, win = 0;
+    __device__ void load_window(int r0) {
+        win = r0;
+        const uint32_t lane = threadIdx.x & 63;
+        idv = __builtin_amdgcn_raw_buffer_load_b32(ids, (int)(((uint32_t)r0 + lane) * (uint32_t)H * 4u), 0, 0);
+        // wait here, once: a wait at the first use inside the loop would also
+        // wait for every checkpoint store issued since
+        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    }
+    // Page id of local row r (uniform; rows are visited in increasing order).
+    __device__ int window_id(int r) {
+        if (r - win >= 64) load_window(r);
+        return __builtin_amdgcn_readlane(idv, r - win);
+    }
+    // Destination of the next checkpoint; id is load_id() or window_id() of its row.
     __device__ float *next(int id) {
         float *d = nullptr;
         if (paged) {

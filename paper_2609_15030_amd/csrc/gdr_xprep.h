@@ -9,18 +9,18 @@
 //   A    = strictly lower part of beta_r exp(Gp_r - G_s) (k_r . k_s)
 //   X    = (I + A)^{-1}                      (unit lower triangular, fp32)
 // With S_0 the state entering the chunk, the corrections
-//   U = X (diag(beta) V - diag(beta exp(Gp)) K S_0)
+//   U = X diag(beta) (V - diag(exp(Gp)) K S_0)
 // hold u_r = beta_r (v_r - pred_r): unrolling the recurrence inside the
 // chunk, the prediction of row r sees S_0 decayed by exp(Gp_r) plus the
 // rank-one writes of the earlier rows s decayed by exp(Gp_r - G_s).  The
 // scan evaluates that product itself; this kernel writes what it needs that
 // the inputs do not hold:
-//   X in bf16 as MFMA A-operand fragments whose columns are permuted the way
+//   X diag(beta) in bf16 as MFMA A-operand fragments whose columns are permuted the way
 //     the scan holds the rows of its C-layout accumulators (perm_row): row
 //     tile mt, k-step ks, lane (g, c): X[16 mt + c][perm_row(8 ks + j, g)],
 //     j < 8.  X is lower triangular, so only k-steps ks <= mt / 2 are stored
 //     (6 fragments of 1 KB: slot xfrag_slot(mt, ks));
-//   the gate block: G, d = beta exp(Gp), beta and exp(G_63 - G), 64 fp32 each.
+//   the gate block: G, exp(Gp), beta and exp(G_63 - G), 64 fp32 each.
 // Both sit in one 7 KB block per chunk-head (X fragments, then the gate
 // block), which the scan copies into LDS as is.
 // Every exponent is a difference formed before exponentiation (<= 0 when
@@ -41,8 +41,8 @@ struct XPrepArgs {
     const float *g, *beta;
     const int32_t *cu;
     int32_t n_seqs, n_heads, C, cps, variant, max_chunks;
-    uint4 *misc;       // per slot-head: X fragments [kXFrags][64 lanes] x 16 B, then
-                       // the gate block [4][64] fp32: G, d, beta, exp(G_63 - G)
+    uint4 *misc;       // per slot-head: X diag(beta) fragments [kXFrags][64 lanes] x 16 B,
+                       // then the gate block [4][64] fp32: G, exp(Gp), beta, exp(G_63 - G)
     int32_t chunk_major;
 };
 
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(256) void gdr_xprep_kernel(XPrepArgs a) {
             sm.bs[lane] = b;
             float *gb = (float *)(a.misc + sh * kMiscVec + kXFrags * 64);
             gb[lane] = x;
-            gb[kChunk + lane] = b * __builtin_amdgcn_exp2f(gp * kLog2e);
+            gb[kChunk + lane] = __builtin_amdgcn_exp2f(gp * kLog2e);
             gb[2 * kChunk + lane] = b;
             gb[3 * kChunk + lane] = __builtin_amdgcn_exp2f((g63 - x) * kLog2e);
         }
@@ -223,7 +223,7 @@ __global__ __launch_bounds__(256) void gdr_xprep_kernel(XPrepArgs a) {
                 const float4 x4 = *(const float4 *)&sm.xm[r][s0];
                 const float xv[4] = {x4.x, x4.y, x4.z, x4.w};
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v8[4 * half + e] = (__bf16)(s0 + e <= r ? xv[e] : 0.f);
+                for (int e = 0; e < 4; ++e) v8[4 * half + e] = (__bf16)(s0 + e <= r ? xv[e] * sm.bs[s0 + e] : 0.f);
             }
             xout[xfrag_slot(mt, ks) * 64 + lane] = *(const uint4 *)v8;
         }

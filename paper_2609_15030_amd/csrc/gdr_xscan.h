@@ -11,8 +11,8 @@
 // and the gate block and X written by the preparation kernel (gdr_xprep.h):
 //
 //   scan wave    Y   = K S_0                      A = K rows, B = S_0
-//                Z   = diag(beta) V - diag(d) Y   d = beta exp(Gp), V in C layout
-//                U   = X Z                        A = X fragments, B = Z
+//                Z   = V - diag(exp(Gp)) Y        V in C layout
+//                U   = X diag(beta) Z             A = X diag(beta) fragments, B = Z
 //                S_1 = exp(G_63) S_0 + K^T diag(exp(G_63 - G)) U
 //   output wave  O^T = scale ((S_0^T Q^T) diag(exp G) + U^T P^T),
 //                P   = (Q K^T) exp(G_r - G_s) on s <= r, zero above
@@ -86,7 +86,7 @@ template <int DK, int CW, bool OUT, int NVB> struct XLds {
     struct Buf {
         uint4 k[KV];                             // K rows, pieces XOR-swizzled by row (xpiece)
         uint4 q[OUT ? KV : 1];                   // Q, same layout
-        uint4 misc[kMiscVec];                    // X fragments, then the gate block
+        uint4 misc[kMiscVec];                    // X diag(beta) fragments, then the gate block
     };
     Buf buf[2];
     uint4 v[NVB][NPAIR][kChunk * 32 / 8];        // each pair's 32 value columns, row-major [64][32]
@@ -310,7 +310,10 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
         }
         float dprod = 1.f;   // product of the chunk decays (the map's D)
         CkptDst ck;
-        if constexpr (MODE == kXScan) ck.init(a, seq, h, len, (size_t)DK * DV, part == 0 && pr == 0);
+        if constexpr (MODE == kXScan) {
+            ck.init(a, seq, h, len, (size_t)DK * DV, part == 0 && pr == 0);
+            ck.load_window(0);
+        }
         uint32_t soff[2];
 #pragma unroll
         for (int c = 0; c < 2; ++c) soff[c] = 4u * (uint32_t)(8 * g16 * DV + pcol + 16 * c + c16);
@@ -337,22 +340,19 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             const typename Lds::Buf &B = sm.buf[bi];
             int lo, hi;
             chunk_range32(jj, len, a.C, a.cps, &lo, &hi);
-            // the page id of a checkpoint this chunk ends on
-            int ckid = 0;
-            if constexpr (MODE == kXScan) {
-                if (hi % a.C == 0) ckid = ck.load_id(hi / a.C - 1);
-            }
 
             // Each phase issues its LDS reads ahead of the MFMAs that use them
             // (sched_barrier keeps the order): one wave per SIMD pair half
             // cannot hide LDS latency otherwise.
             // ---- Y = K S_0: row tiles 0-1's K fragments in flight, then 2-3's
             // behind the first half of the MFMAs
+            const float *gate = (const float *)&B.misc[kXFrags * 64];
             bf16x8 kf[4][KS];
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) kf[mt][ks] = row_frag<DK>(B.k, mt, ks, lane);
+            const float eL = __builtin_amdgcn_exp2f(gate[kChunk - 1] * kLog2e);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int mt = 2; mt < 4; ++mt)
@@ -369,13 +369,11 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
                 }
             __builtin_amdgcn_sched_barrier(0);
             // the reads of Z and U (values, gates, X) behind the second half of Y
-            const float *gate = (const float *)&B.misc[kXFrags * 64];
-            float4 d4[4], b4[4];
+            float4 d4[4];   // exp(Gp) of the lane's rows
             i16x4 vr[2][4];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
                 d4[mt] = *(const float4 *)&gate[kChunk + 16 * mt + 4 * g16];
-                b4[mt] = *(const float4 *)&gate[2 * kChunk + 16 * mt + 4 * g16];
 #pragma unroll
                 for (int c = 0; c < 2; ++c)
                     vr[c][mt] = RowTile<T>::tr4((const T *)&sm.v[bi % NVB][pr][0], 32, 16 * mt + 4 * g16 + ((lane & 15) >> 2), 16 * c, lane);
@@ -383,6 +381,12 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             bf16x8 xf[kXFrags];
 #pragma unroll
             for (int e = 0; e < kXFrags; ++e) xf[e] = __builtin_bit_cast(bf16x8, B.misc[e * 64 + lane]);
+            // exp(G_63) S_0, the state update's starting accumulator, while the
+            // MFMAs of Y run (Y reads S_0 from its bf16 copy)
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int t = 0; t < RT; ++t) S[c][t] = S[c][t] * eL;
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int mt = 2; mt < 4; ++mt)
@@ -400,17 +404,17 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) kt[t][ks] = kt_frag<DK>(B.k, t, ks, lane);
             __builtin_amdgcn_sched_barrier(0);
-            // ---- Z = diag(beta) V - diag(d) Y; U = X Z
+            // ---- Z = V - diag(exp(Gp)) Y; U = X diag(beta) Z
             T zb[2][16];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
                 const float dv[4] = {d4[mt].x, d4[mt].y, d4[mt].z, d4[mt].w};
-                const float bv[4] = {b4[mt].x, b4[mt].y, b4[mt].z, b4[mt].w};
 #pragma unroll
                 for (int c = 0; c < 2; ++c)
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        zb[c][4 * mt + i] = (T)(bv[i] * (float)__builtin_bit_cast(T, (short)vr[c][mt][i]) - dv[i] * Y[c][mt][i]);
+                        zb[c][4 * mt + i] =
+                            (T)__builtin_fmaf(-dv[i], Y[c][mt][i], (float)__builtin_bit_cast(T, (short)vr[c][mt][i]));
             }
             __builtin_amdgcn_sched_barrier(0);
             // the second half's K^T fragments, in flight behind U
@@ -457,13 +461,12 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
                               // values of chunk jj are read, so the helpers may replace them
             }
             // ---- S = exp(G_63) S + K^T diag(exp(G_63 - G)) U
-            const float eL = __builtin_amdgcn_exp2f(gate[kChunk - 1] * kLog2e);
             dprod *= eL;
 #pragma unroll
             for (int t = 0; t < RT; ++t)
 #pragma unroll
                 for (int c = 0; c < 2; ++c) {
-                    f32x4 acc = S[c][t] * eL;
+                    f32x4 acc = S[c][t];
 #pragma unroll
                     for (int ks = 0; ks < 2; ++ks) acc = M::mma(kt[t][ks], M::pack(&ub2[c][8 * ks]), acc);
                     S[c][t] = acc;
@@ -472,7 +475,7 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
                 // checkpoint when the chunk ends on a multiple of C (positions are
                 // local and start on a multiple of C)
                 if (hi % a.C == 0) {
-                    if (float *d = ck.next(ckid)) {
+                    if (float *d = ck.next(ck.window_id(hi / a.C - 1))) {
 #pragma unroll
                         for (int c = 0; c < 2; ++c) store_state_perm<DK, DV>(d, S[c], soff[c]);
                     }
