@@ -645,7 +645,7 @@ def counters_markdown(dirs, steps):
            "| kernel | role | counter | dispatches | mean per dispatch |", "|---|---|---|---|---|"]
     step_vals = {}
     for (c, k), xs in sorted(per.items()):
-        if k.startswith("page_save_kernel"):
+        if not k.startswith(("gdr_xprep_kernel", "gdr_xscan_kernel", "gdr_xcombine_kernel")):
             continue
         sel = xs[len(xs) - steps:] if len(xs) >= steps else xs
         m = statistics.fmean(sel)
@@ -655,7 +655,7 @@ def counters_markdown(dirs, steps):
     stage_of = {"gdr_xprep_kernel": "prep"}
     roles = {}
     for (c, k), m in step_vals.items():
-        if c not in factor:
+        if c not in factor or not k.startswith(("gdr_xprep_kernel", "gdr_xscan_kernel", "gdr_xcombine_kernel")):
             continue
         stage = stage_of.get(k.split("<")[0], "scan")
         key = "read_bytes" if c == "FETCH_SIZE" else "write_bytes"
@@ -669,13 +669,17 @@ def counters_markdown(dirs, steps):
     mops = {k: m for (c, k), m in step_vals.items() if c == "SQ_INSTS_VALU_MFMA_MOPS_BF16"}
     gui = {k: m for (c, k), m in step_vals.items() if c == "GRBM_GUI_ACTIVE"}
     if mops:
-        out += ["", "| kernel | trace avg us (step) | executed bf16 MFMA flops (MOPS x 512) | executed TFLOP/s | "
-                "% of 2,500 | MFMA busy / (GUI_ACTIVE x 1,024 SIMDs) |", "|---|---|---|---|---|---|"]
+        out += ["", "GRBM_GUI_ACTIVE sums the 8 XCDs (it reads 8x the kernel's cycles at 2.4 GHz), so the MFMA "
+                "busy fraction is SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1,024 SIMDs).", "",
+                "| kernel | trace avg us (step) | executed bf16 MFMA flops (MOPS x 512) | executed TFLOP/s | "
+                "% of 2,500 | MFMA busy fraction |", "|---|---|---|---|---|---|"]
         for k, m in sorted(mops.items()):
+            if not k.startswith(("gdr_xprep_kernel", "gdr_xscan_kernel", "gdr_xcombine_kernel")):
+                continue
             ds = dur.get(k, [])
             t = statistics.fmean(ds[len(ds) - steps:]) if ds else float("nan")
             fl = m * 512
-            util = busy.get(k, float("nan")) / (gui.get(k, float("nan")) * 1024) if k in gui else float("nan")
+            util = busy.get(k, float("nan")) / (gui.get(k, float("nan")) / 8 * 1024) if k in gui else float("nan")
             out.append(f"| {k} | {t * 1e6:.2f} | {fl:,.0f} | {fl / t / 1e12:.1f} | "
                        f"{100 * fl / t / 1e12 / BF16_PEAK_TFLOPS:.2f} | {util:.4f} |")
     out += ["", "traffic-record: " + json.dumps(rec)]
