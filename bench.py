@@ -45,6 +45,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import gc
 import glob
 import hashlib
 import json
@@ -143,10 +144,14 @@ def measured_traffic(role):
     return None if r is None else r["read_bytes"] + r["write_bytes"]
 
 
+SPIN_CYCLES = 100_000_000   # ~40 ms of GPU spin ahead of each timed loop
+
+
 class Timer:
     """Per-repetition HIP-event intervals on one stream.  All repetitions are
-    queued behind a GPU spin before the first event is read, so the host's
-    launch latency never sits inside an interval."""
+    queued behind a GPU spin before the first event is read (with Python's
+    garbage collector paused), so the host's launch latency and its pauses
+    stay outside the intervals."""
 
     def __init__(self, torch, stream_ptr):
         self.torch = torch
@@ -169,12 +174,16 @@ class Timer:
         included) is kept in ``last_span_ms``."""
         ev = HipEvents(2 * reps)
         self.torch.cuda.synchronize()
-        self.torch.cuda._sleep(20_000_000)
-        for r in range(reps):
-            self.flush()
-            ev.record(2 * r, self.sp)
-            run()
-            ev.record(2 * r + 1, self.sp)
+        gc.disable()
+        try:
+            self.torch.cuda._sleep(SPIN_CYCLES)
+            for r in range(reps):
+                self.flush()
+                ev.record(2 * r, self.sp)
+                run()
+                ev.record(2 * r + 1, self.sp)
+        finally:
+            gc.enable()
         self.last_span_ms = ev.ms(0, 2 * reps - 1)
         return [ev.ms(2 * r, 2 * r + 1) for r in range(reps)]
 
@@ -182,12 +191,16 @@ class Timer:
         """Per-repetition ms over back-to-back repetitions (no flush)."""
         ev = HipEvents(2 * reps)
         self.torch.cuda.synchronize()
-        self.torch.cuda._sleep(20_000_000)
-        run()
-        for r in range(reps):
-            ev.record(2 * r, self.sp)
+        gc.disable()
+        try:
+            self.torch.cuda._sleep(SPIN_CYCLES)
             run()
-            ev.record(2 * r + 1, self.sp)
+            for r in range(reps):
+                ev.record(2 * r, self.sp)
+                run()
+                ev.record(2 * r + 1, self.sp)
+        finally:
+            gc.enable()
         return [ev.ms(2 * r, 2 * r + 1) for r in range(reps)]
 
     def stages(self, la, run, reps):
@@ -212,11 +225,22 @@ def summary(ms):
             "mean_us": round(statistics.fmean(ms) * 1e3, 2), "reps": len(ms)}
 
 
-FORM_KERNELS = {1: {"prep": ["gdr_xprep_kernel"], "maps_combine": [],
-                    "scan": ["gdr_xscan_kernel<128, 128, 0>"]},
-                2: {"prep": ["gdr_xprep_kernel"],
-                    "maps_combine": ["gdr_xscan_kernel<128, 128, 2>", "gdr_xcombine_kernel<128, 128>"],
-                    "scan": ["gdr_xscan_kernel<128, 128, 1>"]}}
+def scan_width(units, ncols=128):
+    """Columns per fused-scan workgroup for `units` independent units (the
+    library's choice for dk = dv = 128: 128 while that still gives each of
+    the 256 CUs two workgroups, else 64)."""
+    return 128 if units * (ncols // 128) >= 2 * 256 else 64
+
+
+def form_kernels(form, units):
+    w = scan_width(units)
+    if form == 1:
+        return {"prep": ["gdr_xprep_kernel<128>"], "maps_combine": [],
+                "scan": [f"gdr_xscan_kernel<128, 128, 0, {w}>"]}
+    return {"prep": ["gdr_xprep_kernel<128>"],
+            "maps_combine": [f"gdr_xscan_kernel<128, 128, 2, {scan_width(units, 256)}>",
+                             "gdr_xcombine_kernel<128, 128>"],
+            "scan": [f"gdr_xscan_kernel<128, 128, 1, {w}>"]}
 
 
 class VarlenStep:
@@ -560,8 +584,8 @@ def roofline_of(v, la, stages, dk, dv, tokens):
     dur = stages["prep"] if dom == "prep" else scan_ms
     flops = fl[dom] * tokens * v.H
     achieved = flops / (dur * 1e-3) / 1e12
-    kernels = FORM_KERNELS[form][dom] if dom == "prep" else \
-        FORM_KERNELS[form]["maps_combine"] + FORM_KERNELS[form]["scan"]
+    fk = form_kernels(form, len(v.lens) * v.H)
+    kernels = fk[dom] if dom == "prep" else fk["maps_combine"] + fk["scan"]
     return {"bound": "mfma", "kernel": " + ".join(kernels), "achieved": round(achieved, 3),
             "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 5),
             "traffic": measured_traffic("step " + dom),
