@@ -53,6 +53,8 @@
 #include "gdr_scan.h"
 #include "gdr_xprep.h"
 
+#include <type_traits>
+
 namespace la {
 
 enum : int { kXScan = 0, kXReplay = 1, kXMap = 2 };
@@ -520,25 +522,31 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
         }
     } else if (role == 2) {
         // ================================ loader wave ================================
-        // (kLoad3) Stages chunk jj + 1's inputs at the start of chunk jj, from
-        // registers loaded during chunk jj - 1, then loads chunk jj + 2's.
-        // The buffers written were last read in chunk jj - 1.
+        // (kLoad3) Two register sets, by chunk parity P: during chunk jj the
+        // loader issues the global loads of chunk jj + 2 into set P (whose
+        // chunk jj is already in LDS) before B_jj, and after B_jj, beside the
+        // state update, stores chunk jj + 1 (set P ^ 1, loaded during chunk
+        // jj - 1) into the other LDS buffers, last read in chunk jj - 1.
         if constexpr (kLoad3) {
-            Stage st;
-            stage_load(st, c0);
-            stage_store_shared(st, 0);
-            stage_store_values(st, 0);
-            if (c0 + 1 < c1) stage_load(st, c0 + 1);
+            Stage st[2];
+            stage_load(st[0], c0);
+            stage_store_shared(st[0], 0);
+            stage_store_values(st[0], 0);
+            if (c0 + 1 < c1) stage_load(st[1], c0 + 1);
             xbar_lds();
-            for (int jj = c0; jj < c1; ++jj) {
-                const int bi = (jj - c0) & 1;
-                if (jj + 1 < c1) {
-                    stage_store_shared(st, bi ^ 1);
-                    stage_store_values(st, bi ^ 1);
-                }
-                if (jj + 2 < c1) stage_load(st, jj + 2);
+            auto chunk = [&](auto parity, int jj) {
+                constexpr int P = decltype(parity)::value;
+                if (jj + 2 < c1) stage_load(st[P], jj + 2);
                 xbar_lds();   // B_jj
+                if (jj + 1 < c1) {
+                    stage_store_shared(st[P ^ 1], P ^ 1);
+                    stage_store_values(st[P ^ 1], P ^ 1);
+                }
                 xbar_lds();   // C_jj
+            };
+            for (int jj = c0; jj < c1; jj += 2) {
+                chunk(std::integral_constant<int, 0>{}, jj);
+                if (jj + 1 < c1) chunk(std::integral_constant<int, 1>{}, jj + 1);
             }
         }
     } else {
