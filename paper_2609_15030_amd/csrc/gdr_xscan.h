@@ -3,11 +3,11 @@
 // workgroup in LDS.
 //
 // A workgroup owns CW state columns of one (sequence, head) and runs its
-// chunks in order.  Each 32 of its columns (two 16-column tiles) belong to
-// a pair of waves on one SIMD: a scan wave, which keeps those columns of the
-// fp32 state in MFMA result registers for the whole run, and (when the unit
-// has an output) an output wave, which reads the output out beside it and
-// fills the scan wave's stalls.  Per chunk, with S_0 the state entering it
+// chunks in order.  Each 32 of its columns (two 16-column tiles; in the
+// 32-column form each 16) belong to a pair of waves: a scan wave, which
+// keeps those columns of the fp32 state in MFMA result registers for the
+// whole run, and (when the unit has an output) an output wave, which reads
+// the output out beside it.  Per chunk, with S_0 the state entering it
 // and the gate block and X written by the preparation kernel (gdr_xprep.h):
 //
 //   scan wave    Y   = K S_0                      A = K rows, B = S_0
@@ -59,19 +59,24 @@ namespace la {
 
 enum : int { kXScan = 0, kXReplay = 1, kXMap = 2 };
 
-// Waves per workgroup: a scan wave and a helper per 32-column pair.  The
-// 64-column form with an output gives each pair a third wave: one helper
+// Column tiles per wave (16 columns each) and wave pairs per workgroup:
+// the 32-column form gives each wave one tile, the wider forms two.
+constexpr int xscan_tw(int cw) { return cw == 32 ? 1 : 2; }
+constexpr int xscan_npair(int cw) { return cw / (16 * xscan_tw(cw)); }
+// Waves per workgroup: a scan wave and a helper per pair.  The 32- and
+// 64-column forms with an output give each pair a third wave: one helper
 // then reads the output out and the other (the loader) stages the inputs.
-constexpr bool xscan_loaders(int cw, int mode) { return cw == 64 && mode != kXMap; }
-constexpr int xscan_threads(int cw, int mode) { return 64 * (cw / 32) * (xscan_loaders(cw, mode) ? 3 : 2); }
+constexpr bool xscan_loaders(int cw, int mode) { return cw <= 64 && mode != kXMap; }
+constexpr int xscan_threads(int cw, int mode) { return 64 * xscan_npair(cw) * (xscan_loaders(cw, mode) ? 3 : 2); }
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
-// Columns per workgroup (CW): 128 (four wave pairs) or 64 (two).  Every
-// column's arithmetic is the same whatever CW, so the choice is free: 64
-// spreads a chain over more CUs when there are few chains, 128 stages each
-// chunk's K, Q and prepared block once for twice the columns.  The map's Phi
-// and R parts split at a part boundary, so CW divides dk.
+// Columns per workgroup (CW): 128 (four wave pairs of 32 columns), 64 (two)
+// or 32 (two pairs of 16).  Every column's arithmetic is the same whatever
+// CW, so the choice is free: narrower workgroups spread a chain over more
+// CUs and shorten each chunk's step when there are few chains, 128 stages
+// each chunk's K, Q and prepared block once for twice the columns.  The
+// map's Phi and R parts split at a part boundary, so CW divides dk.
 
 // dk row held at state tile-row x = 16 t + 4 g + q (lane group g, element
 // q of tile t): the B-operand contraction index 8 ks + j of lane group g
@@ -83,7 +88,7 @@ __device__ __host__ inline int state_row(int x) {
 }
 
 template <int DK, int CW, bool OUT, int NVB> struct XLds {
-    static constexpr int NPAIR = CW / 32;
+    static constexpr int TW = xscan_tw(CW), NPAIR = xscan_npair(CW), PW = 16 * TW;
     static constexpr int KV = kChunk * DK / 8;   // 16-byte pieces of a chunk's K (or Q)
     struct Buf {
         uint4 k[KV];                             // K rows, pieces XOR-swizzled by row (xpiece)
@@ -91,11 +96,11 @@ template <int DK, int CW, bool OUT, int NVB> struct XLds {
         uint4 misc[kMiscVec];                    // X diag(beta) fragments, then the gate block
     };
     Buf buf[2];
-    uint4 v[NVB][NPAIR][kChunk * 32 / 8];        // each pair's 32 value columns, row-major [64][32]
+    uint4 v[NVB][NPAIR][kChunk * PW / 8];        // each pair's PW value columns, row-major [64][PW]
                                                  // (double-buffered when loader waves stage them)
     uint4 pf[OUT ? 4 * 2 * 64 : 1];              // P fragments [row tile][k-step][lane]
-    uint4 sbh[OUT ? NPAIR : 1][2][DK / 32][64];  // S_0 handed to the output wave (B-operand fragments)
-    uint4 ubh[OUT ? NPAIR : 1][2][2][64];        // U handed to the output wave
+    uint4 sbh[OUT ? NPAIR : 1][TW][DK / 32][64]; // S_0 handed to the output wave (B-operand fragments)
+    uint4 ubh[OUT ? NPAIR : 1][TW][2][64];       // U handed to the output wave
 };
 
 // Physical 16-byte piece of logical piece p in row r of a K or Q tile (DK / 8
@@ -141,13 +146,13 @@ __device__ inline void xbar_lds() {
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
-// Start state of a wave's two column tiles (permuted rows) from a row-major
+// Start state of a wave's TW column tiles (permuted rows) from a row-major
 // [DK][DV] fp32 state, or zero.
-template <int DK, int DV>
-__device__ inline void load_state_perm(const float *src, int col0, f32x4 (&S)[2][DK / 16]) {
+template <int DK, int DV, int TW>
+__device__ inline void load_state_perm(const float *src, int col0, f32x4 (&S)[TW][DK / 16]) {
     const int lane = threadIdx.x & 63, g16 = lane >> 4, c16 = lane & 15;
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < TW; ++c)
 #pragma unroll
         for (int t = 0; t < DK / 16; ++t)
 #pragma unroll
@@ -172,9 +177,11 @@ template <int DK, int DV, int MODE, int CW>
 __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(ScanArgs a) {
     using M = MT<__bf16>;
     typedef __bf16 T;
-    static_assert(CW == 64 || CW == 128, "column width");
+    static_assert(CW == 32 || CW == 64 || CW == 128, "column width");
     constexpr bool kOut = MODE != kXMap;
-    constexpr int NPAIR = CW / 32;                     // scan waves (and output waves with kOut)
+    constexpr int TW = xscan_tw(CW);                   // column tiles per wave
+    constexpr int NPAIR = xscan_npair(CW);             // scan waves (and output waves with kOut)
+    constexpr int PW = 16 * TW;                        // state columns per pair
     constexpr int NTH = xscan_threads(CW, MODE);
     constexpr bool kLoad3 = xscan_loaders(CW, MODE);   // loader waves of their own
     constexpr int RT = DK / 16, FS = DK / 4, KS = DK / 32;
@@ -222,30 +229,34 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
     const int cb = part * CW;                          // first column of the part
     const bool phi = MODE == kXMap && cb < DK;         // a part of Phi (identity start, no values)
     const int vcol0 = (MODE == kXMap) ? cb - DK : cb;  // first value (state) column of the part
-    const int pcol = vcol0 + 32 * pr;                  // first state column of the wave's pair
+    const int pcol = vcol0 + PW * pr;                  // first state column of the wave's pair
 
     // ---- staging of chunk jj's inputs by the helper waves (the output
     // waves, or in the map loader waves of their own): global loads into
     // registers (rows past the chunk's end read as zero through the buffer
     // range), then 16-byte LDS stores.  Helper wave p stages a quarter of K,
-    // Q and the preparation's block, and pair p's 32 value columns.  The scan
+    // Q and the preparation's block, and pair p's PW value columns.  The scan
     // waves issue no global loads, so nothing they read from LDS waits on a
     // load in flight.
     constexpr int KPW = KV / 64 / NPAIR;                 // 16-byte pieces of K per helper lane
     constexpr int MPW = (kMiscVec + 64 * NPAIR - 1) / (64 * NPAIR);
-    constexpr int VPW = kChunk * 32 / 8 / 64;            // pieces of a pair's values per lane (4)
+    constexpr int VPR = PW / 8;                          // 16-byte pieces of a value row of a pair
+    constexpr int VPW = kChunk * VPR / 64;               // pieces of a pair's values per lane
     static_assert(KPW * 64 * NPAIR == KV, "K staging tiling");
     struct Stage {
         uint4 k[KPW], q[kOut ? KPW : 1], m[MPW], v[VPW];
     };
     const T *qin = (const T *)a.q, *kin = (const T *)a.k, *vin = (const T *)a.v;
     const bool has_v = !phi;
+    // A chunk past the run's last has empty ranges: its loads read zero and
+    // touch no memory, so a loader can issue them unconditionally.
     auto stage_load = [&](Stage &st, int jj) {
-        int lo, hi;
-        chunk_range32(jj, len, a.C, a.cps, &lo, &hi);
+        const bool live = jj < c1;
+        int lo = 0, hi = 0;
+        if (live) chunk_range32(jj, len, a.C, a.cps, &lo, &hi);
         const int n = hi - lo;
         const int64_t row0 = ((int64_t)cu0 + lo) * H + h;
-        const uint32_t rows_k = head_rows_bytes<T>(n, H, DK);
+        const uint32_t rows_k = live ? head_rows_bytes<T>(n, H, DK) : 0u;
         const auto rk = make_rsrc(kin + row0 * DK, rows_k);
         const auto rq = make_rsrc(qin + row0 * DK, rows_k);
 #pragma unroll
@@ -255,16 +266,16 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             st.k[it] = buf_load16(rk, voff, 0u);
             if constexpr (kOut) st.q[it] = buf_load16(rq, voff, 0u);
         }
-        const auto rm = make_rsrc(a.ws.misc + ((base + jj) * H + h) * kMiscVec, kMiscVec * 16);
+        const auto rm = make_rsrc(a.ws.misc + ((base + jj) * H + h) * kMiscVec, live ? kMiscVec * 16 : 0u);
 #pragma unroll
         for (int it = 0; it < MPW; ++it)
             st.m[it] = buf_load16(rm, (uint32_t)(((pr * MPW + it) * 64 + lane) * 16), 0u);
         const uint32_t vbytes =
-            has_v ? (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)((n - 1) * H * DV + 32) * 2)) : 0u;
+            (has_v && live) ? (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)((n - 1) * H * DV + PW) * 2)) : 0u;
         const auto rv = make_rsrc(vin + row0 * DV + pcol, vbytes);
 #pragma unroll
         for (int it = 0; it < VPW; ++it) {
-            const int e = it * 64 + lane, r = e >> 2, p = e & 3;
+            const int e = it * 64 + lane, r = e / VPR, p = e % VPR;
             st.v[it] = buf_load16(rv, (uint32_t)(r * H * DV * 2 + 16 * p), 0u);
         }
     };
@@ -294,19 +305,19 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
 
     if (scan_wave) {
         // ================================ scan wave ================================
-        f32x4 S[2][RT];
+        f32x4 S[TW][RT];
         if constexpr (MODE == kXMap) {
 #pragma unroll
-            for (int c = 0; c < 2; ++c)
+            for (int c = 0; c < TW; ++c)
 #pragma unroll
                 for (int t = 0; t < RT; ++t)
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        S[c][t][i] = (phi && state_row(16 * t + 4 * g16 + i) == cb + 32 * pr + 16 * c + c16) ? 1.f : 0.f;
+                        S[c][t][i] = (phi && state_row(16 * t + 4 * g16 + i) == cb + PW * pr + 16 * c + c16) ? 1.f : 0.f;
         } else if (MODE == kXReplay && sg > 0) {
             const float *src = a.seg.state + (seg_slot * H + h) * DK * DV;
 #pragma unroll
-            for (int c = 0; c < 2; ++c) load_state_c<RT>(src, pcol / 16 + c, S[c]);
+            for (int c = 0; c < TW; ++c) load_state_c<RT>(src, pcol / 16 + c, S[c]);
         } else {
             load_state_perm<DK, DV>(start_state(a, seq, h, (size_t)DK * DV, part == 0 && pr == 0), pcol, S);
         }
@@ -316,20 +327,20 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             ck.init(a, seq, h, len, (size_t)DK * DV, part == 0 && pr == 0);
             ck.load_window(0);
         }
-        uint32_t soff[2];
+        uint32_t soff[TW];
 #pragma unroll
-        for (int c = 0; c < 2; ++c) soff[c] = 4u * (uint32_t)(8 * g16 * DV + pcol + 16 * c + c16);
+        for (int c = 0; c < TW; ++c) soff[c] = 4u * (uint32_t)(8 * g16 * DV + pcol + 16 * c + c16);
 
         // S_0 as bf16 B operand (k-step ks: dk 32 ks + 8 g .. + 7)
-        T sb[2][FS];
+        T sb[TW][FS];
         auto make_sb = [&]() {
 #pragma unroll
-            for (int c = 0; c < 2; ++c)
+            for (int c = 0; c < TW; ++c)
 #pragma unroll
                 for (int f = 0; f < FS; ++f) sb[c][f] = (T)S[c][f >> 2][f & 3];
             if constexpr (kOut) {
 #pragma unroll
-                for (int c = 0; c < 2; ++c)
+                for (int c = 0; c < TW; ++c)
 #pragma unroll
                     for (int ks = 0; ks < KS; ++ks) sm.sbh[pr][c][ks][lane] = *(const uint4 *)&sb[c][8 * ks];
             }
@@ -360,11 +371,11 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             for (int mt = 2; mt < 4; ++mt)
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) kf[mt][ks] = row_frag<DK>(B.k, mt, ks, lane);
-            f32x4 Y[2][4];
+            f32x4 Y[TW][4];
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-                for (int c = 0; c < 2; ++c) {
+                for (int c = 0; c < TW; ++c) {
                     Y[c][mt] = zero4();
 #pragma unroll
                     for (int ks = 0; ks < KS; ++ks) Y[c][mt] = M::mma(kf[mt][ks], M::pack(&sb[c][8 * ks]), Y[c][mt]);
@@ -372,13 +383,13 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             __builtin_amdgcn_sched_barrier(0);
             // the reads of Z and U (values, gates, X) behind the second half of Y
             float4 d4[4];   // exp(Gp) of the lane's rows
-            i16x4 vr[2][4];
+            i16x4 vr[TW][4];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
                 d4[mt] = *(const float4 *)&gate[kChunk + 16 * mt + 4 * g16];
 #pragma unroll
-                for (int c = 0; c < 2; ++c)
-                    vr[c][mt] = RowTile<T>::tr4((const T *)&sm.v[bi % NVB][pr][0], 32, 16 * mt + 4 * g16 + ((lane & 15) >> 2), 16 * c, lane);
+                for (int c = 0; c < TW; ++c)
+                    vr[c][mt] = RowTile<T>::tr4((const T *)&sm.v[bi % NVB][pr][0], PW, 16 * mt + 4 * g16 + ((lane & 15) >> 2), 16 * c, lane);
             }
             bf16x8 xf[kXFrags];
 #pragma unroll
@@ -386,14 +397,14 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             // exp(G_63) S_0, the state update's starting accumulator, while the
             // MFMAs of Y run (Y reads S_0 from its bf16 copy)
 #pragma unroll
-            for (int c = 0; c < 2; ++c)
+            for (int c = 0; c < TW; ++c)
 #pragma unroll
                 for (int t = 0; t < RT; ++t) S[c][t] = S[c][t] * eL;
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int mt = 2; mt < 4; ++mt)
 #pragma unroll
-                for (int c = 0; c < 2; ++c) {
+                for (int c = 0; c < TW; ++c) {
                     Y[c][mt] = zero4();
 #pragma unroll
                     for (int ks = 0; ks < KS; ++ks) Y[c][mt] = M::mma(kf[mt][ks], M::pack(&sb[c][8 * ks]), Y[c][mt]);
@@ -407,12 +418,12 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
                 for (int ks = 0; ks < 2; ++ks) kt[t][ks] = kt_frag<DK>(B.k, t, ks, lane);
             __builtin_amdgcn_sched_barrier(0);
             // ---- Z = V - diag(exp(Gp)) Y; U = X diag(beta) Z
-            T zb[2][16];
+            T zb[TW][16];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
                 const float dv[4] = {d4[mt].x, d4[mt].y, d4[mt].z, d4[mt].w};
 #pragma unroll
-                for (int c = 0; c < 2; ++c)
+                for (int c = 0; c < TW; ++c)
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
                         zb[c][4 * mt + i] =
@@ -425,28 +436,28 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) kt[t][ks] = kt_frag<DK>(B.k, t, ks, lane);
             __builtin_amdgcn_sched_barrier(0);
-            f32x4 U[2][4];
+            f32x4 U[TW][4];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-                for (int c = 0; c < 2; ++c) {
+                for (int c = 0; c < TW; ++c) {
                     U[c][mt] = zero4();
 #pragma unroll
                     for (int ks = 0; ks <= (mt >> 1); ++ks)
                         U[c][mt] = M::mma(xf[xfrag_slot(mt, ks)], M::pack(&zb[c][8 * ks]), U[c][mt]);
                 }
             // ---- U to the output wave (unscaled), and diag(exp(G_63 - G)) U
-            T ub2[2][16];
+            T ub2[TW][16];
             {
                 float4 e4[4];
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt) e4[mt] = *(const float4 *)&gate[3 * kChunk + 16 * mt + 4 * g16];
-                T ub[2][16];
+                T ub[TW][16];
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt) {
                     const float ev[4] = {e4[mt].x, e4[mt].y, e4[mt].z, e4[mt].w};
 #pragma unroll
-                    for (int c = 0; c < 2; ++c)
+                    for (int c = 0; c < TW; ++c)
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
                             ub[c][4 * mt + i] = (T)U[c][mt][i];
@@ -455,7 +466,7 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
                 }
                 if constexpr (kOut) {
 #pragma unroll
-                    for (int c = 0; c < 2; ++c)
+                    for (int c = 0; c < TW; ++c)
 #pragma unroll
                         for (int ks = 0; ks < 2; ++ks) sm.ubh[pr][c][ks][lane] = *(const uint4 *)&ub[c][8 * ks];
                 }
@@ -467,7 +478,7 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
 #pragma unroll
             for (int t = 0; t < RT; ++t)
 #pragma unroll
-                for (int c = 0; c < 2; ++c) {
+                for (int c = 0; c < TW; ++c) {
                     f32x4 acc = S[c][t];
 #pragma unroll
                     for (int ks = 0; ks < 2; ++ks) acc = M::mma(kt[t][ks], M::pack(&ub2[c][8 * ks]), acc);
@@ -479,7 +490,7 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
                 if (hi % a.C == 0) {
                     if (float *d = ck.next(ck.window_id(hi / a.C - 1))) {
 #pragma unroll
-                        for (int c = 0; c < 2; ++c) store_state_perm<DK, DV>(d, S[c], soff[c]);
+                        for (int c = 0; c < TW; ++c) store_state_perm<DK, DV>(d, S[c], soff[c]);
                     }
                 }
             }
@@ -491,15 +502,15 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
         if constexpr (MODE == kXScan) {
             if (a.final_state) {
 #pragma unroll
-                for (int c = 0; c < 2; ++c)
+                for (int c = 0; c < TW; ++c)
                     store_state_perm<DK, DV>(a.final_state + (size_t)pair * DK * DV, S[c], soff[c]);
             }
         }
         if constexpr (MODE == kXMap) {
             const int64_t ssh = seg_slot * H + h;
 #pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                const int col = cb + 32 * pr + 16 * c + c16;
+            for (int c = 0; c < TW; ++c) {
+                const int col = cb + PW * pr + 16 * c + c16;
                 if (phi) {
                     // Phi' = Phi - D I, row-major [DK][DK] in the io type
                     T *dst = (T *)a.seg.phi + ssh * DK * DK + col;
@@ -532,11 +543,11 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             stage_load(st[0], c0);
             stage_store_shared(st[0], 0);
             stage_store_values(st[0], 0);
-            if (c0 + 1 < c1) stage_load(st[1], c0 + 1);
+            stage_load(st[1], c0 + 1);
             xbar_lds();
-            auto chunk = [&](auto parity, int jj) {
+            auto chunk = [&](auto parity, int jj) __attribute__((always_inline)) {
                 constexpr int P = decltype(parity)::value;
-                if (jj + 2 < c1) stage_load(st[P], jj + 2);
+                stage_load(st[P], jj + 2);   // unconditional: st[P] is dead until then
                 xbar_lds();   // B_jj
                 if (jj + 1 < c1) {
                     stage_store_shared(st[P ^ 1], P ^ 1);
@@ -571,15 +582,15 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             if constexpr (!kLoad3) {
                 if (jj + 1 < c1) stage_load(st, jj + 1);
             }
-            [[maybe_unused]] f32x4 O[2][4];   // S_0^T Q^T, finished after B_jj
+            [[maybe_unused]] f32x4 O[TW][4];   // S_0^T Q^T, finished after B_jj
             if constexpr (kOut) {
                 // S_0 handed over at the end of the previous chunk, the Q fragments
                 // and the K fragments of this wave's P tiles, all in flight first.
                 // P tiles (mt, nt), nt <= mt: tile index mt (mt + 1) / 2 + nt,
                 // dealt to the output waves round-robin.
-                bf16x8 sb[2][KS], qf[4][KS];
+                bf16x8 sb[TW][KS], qf[4][KS];
 #pragma unroll
-                for (int c = 0; c < 2; ++c)
+                for (int c = 0; c < TW; ++c)
 #pragma unroll
                     for (int ks = 0; ks < KS; ++ks) sb[c][ks] = __builtin_bit_cast(bf16x8, sm.sbh[pr][c][ks][lane]);
 #pragma unroll
@@ -600,7 +611,7 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-                    for (int c = 0; c < 2; ++c) {
+                    for (int c = 0; c < TW; ++c) {
                         O[c][mt] = zero4();
 #pragma unroll
                         for (int ks = 0; ks < KS; ++ks) O[c][mt] = M::mma(sb[c][ks], qf[mt][ks], O[c][mt]);
@@ -658,9 +669,9 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             xbar_lds();   // B_jj
             if constexpr (kOut) {
                 // ---- O^T = scale ((S_0^T Q^T) diag(exp G) + U^T P^T), 4 columns per lane
-                bf16x8 ubf[2][2], pfr[kXFrags];
+                bf16x8 ubf[TW][2], pfr[kXFrags];
 #pragma unroll
-                for (int c = 0; c < 2; ++c)
+                for (int c = 0; c < TW; ++c)
 #pragma unroll
                     for (int ks = 0; ks < 2; ++ks) ubf[c][ks] = __builtin_bit_cast(bf16x8, sm.ubh[pr][c][ks][lane]);
 #pragma unroll
@@ -677,7 +688,7 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-                    for (int c = 0; c < 2; ++c) {
+                    for (int c = 0; c < TW; ++c) {
                         f32x4 acc = O[c][mt] * eg[mt];
 #pragma unroll
                         for (int ks = 0; ks <= (mt >> 1); ++ks) acc = M::mma(ubf[c][ks], pfr[xfrag_slot(mt, ks)], acc);

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <functional>
 #include <mutex>
 #include <type_traits>
 #include <cmath>
@@ -258,12 +259,60 @@ la::ScanArgs scan_args(const PrefillCall &c, const la::Workspace &ws) {
     return sa;
 }
 
-// The fused scan kernel of one mode over `units` independent units, at the
-// column width that still gives every CU two workgroups (128 columns), else
-// at 64 columns, which spreads each unit over more CUs.  The width never
-// changes a result: every column's arithmetic is the same at both.
+// Per-chunk step of one fused-scan workgroup by column width, relative to
+// the 64-column form's (measured on the MI355X at dk = dv = 128): narrower
+// workgroups give each wave fewer columns, so a chunk takes less time, but
+// a chain then needs more workgroups.
+constexpr double kStep32 = 0.87, kStep64 = 1.0;
+
+// Estimated span of a fused scan whose n chains have nch[0] >= nch[1] >=
+// ... chunks, np workgroups per chain, each holding a CU of its own (their
+// LDS allows one per CU) for its chain's chunks at `step` per chunk: the
+// workgroups dispatch in that order, each onto the first CU to come free.
+double scan_span(const int64_t *nch, int64_t n, int np, double step) {
+    double free_at[kDeviceCUs];   // min-heap of the CUs' free times
+    int64_t used = 0;
+    double span = 0.0;
+    for (int64_t i = 0; i < n; ++i)
+        for (int p = 0; p < np; ++p) {
+            double t = (double)nch[i] * step;
+            if (used == kDeviceCUs) {
+                std::pop_heap(free_at, free_at + used, std::greater<double>());
+                t += free_at[--used];
+            }
+            free_at[used++] = t;
+            std::push_heap(free_at, free_at + used, std::greater<double>());
+            span = std::max(span, t);
+        }
+    return span;
+}
+
+// Column width of the single-level fused scan (bf16, dk = dv = 128) for a
+// call: 128 columns when the chains give every CU two workgroups, else the
+// narrower of 32 and 64 columns whose estimated span is shorter.  Other
+// head sizes take 64.  The width never changes a result.
+int fused_scan_width(const PrefillCall &c) {
+    const la_shape *s = c.shape;
+    const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
+    if (s->dk != 128 || s->dv != 128) return 64;
+    if (pairs >= 2 * kDeviceCUs) return 128;
+    const int cps = la::chunks_per_interval(s->ckpt_interval);
+    int64_t nch[2 * kDeviceCUs];
+    for (int64_t k = 0; k < pairs; ++k) {
+        const int i = (int)(k / s->n_heads);
+        nch[k] = la::n_chunks((int64_t)c.cu_host[i + 1] - c.cu_host[i], s->ckpt_interval, cps);
+    }
+    std::sort(nch, nch + pairs, std::greater<int64_t>());
+    return scan_span(nch, pairs, s->dv / 32, kStep32) < scan_span(nch, pairs, s->dv / 64, kStep64) ? 32 : 64;
+}
+
+// The fused scan kernel of one mode over `units` independent units at
+// column width cw (single-level scan), or, for the two-level passes, at the
+// width that still gives every CU two workgroups (128 columns), else at 64
+// columns, which spreads each unit over more CUs.  The width never changes
+// a result: every column's arithmetic is the same at all widths.
 template <int DK, int DV, int MODE>
-la_status launch_xscan(const la::ScanArgs &sa, int64_t units, hipStream_t stream, const char *what) {
+la_status launch_xscan(const la::ScanArgs &sa, int64_t units, hipStream_t stream, const char *what, int cw = 0) {
     constexpr int NCOLS = MODE == la::kXMap ? DK + DV : DV;
     auto go = [&](auto width) {
         constexpr int CW = decltype(width)::value;
@@ -273,7 +322,11 @@ la_status launch_xscan(const la::ScanArgs &sa, int64_t units, hipStream_t stream
         return hip_check(what);
     };
     if constexpr (DK == 128 && DV == 128) {
-        if (units * (NCOLS / 128) >= 2 * kDeviceCUs) return go(std::integral_constant<int, 128>{});
+        if constexpr (MODE == la::kXScan) {
+            if (cw == 32) return go(std::integral_constant<int, 32>{});
+        }
+        if (cw == 128 || (cw == 0 && units * (NCOLS / 128) >= 2 * kDeviceCUs))
+            return go(std::integral_constant<int, 128>{});
     }
     return go(std::integral_constant<int, 64>{});
 }
@@ -319,7 +372,9 @@ la_status launch_fused(const PrefillCall &c, const WsPlan &p, int64_t max_chunks
                 return e;
     } else {
         trace_mark(2, c.stream);
-        if (la_status e = launch_xscan<DK, DV, la::kXScan>(sa, pairs, c.stream, "fused scan launch")) return e;
+        if (la_status e = launch_xscan<DK, DV, la::kXScan>(sa, pairs, c.stream, "fused scan launch",
+                                                           fused_scan_width(c)))
+            return e;
     }
     trace_mark(3, c.stream);
     return LA_OK;
@@ -357,7 +412,7 @@ la_status launch_f32(const PrefillCall &c, const WsPlan &p, int64_t max_chunks) 
     constexpr int NT = DV / 16;
     const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
     const int64_t blocks = 8 * NT * ((pairs + 7) / 8);
-    if (prefill_form(s) == LA_FORM_TILE_SCAN_OUT) {
+    if constexpr (DK != 128) {   // LA_FORM_TILE_SCAN_OUT (the dk = 128 kernels are not built for it)
         // the scan's output wave produces the output: no output launch
         trace_mark(2, c.stream);
         hipLaunchKernelGGL((la::gdr_scan1o_kernel<T, DK, DV>), dim3((unsigned)blocks), dim3(128), 0, c.stream, sa);
