@@ -225,20 +225,18 @@ def summary(ms):
             "mean_us": round(statistics.fmean(ms) * 1e3, 2), "reps": len(ms)}
 
 
-def scan_width(units, ncols=128):
-    """Columns per fused-scan workgroup for `units` independent units (the
-    library's choice for dk = dv = 128: 128 while that still gives each of
-    the 256 CUs two workgroups, else 64)."""
-    return 128 if units * (ncols // 128) >= 2 * 256 else 64
-
-
-def form_kernels(form, units):
-    w = scan_width(units)
-    if form == 1:
+def form_kernels(la, shape, cu_host, max_segments=1):
+    """Kernel names of a bf16 call (dk = dv = 128): the fused scan's width is
+    the library's choice for these lengths; the segment maps of the
+    two-level form take 128 columns while their units give each of the 256
+    CUs two workgroups, else 64."""
+    w = la.la_prefill_scan_columns(shape, cu_host)
+    if la.la_prefill_form(shape) == la.LA_FORM_FUSED_SCAN:
         return {"prep": ["gdr_xprep_kernel<128>"], "maps_combine": [],
                 "scan": [f"gdr_xscan_kernel<128, 128, 0, {w}>"]}
+    units = shape.n_seqs * shape.n_heads * max_segments
     return {"prep": ["gdr_xprep_kernel<128>"],
-            "maps_combine": [f"gdr_xscan_kernel<128, 128, 2, {scan_width(units, 256)}>",
+            "maps_combine": [f"gdr_xscan_kernel<128, 128, 2, {128 if units * 2 >= 512 else 64}>",
                              "gdr_xcombine_kernel<128, 128>"],
             "scan": [f"gdr_xscan_kernel<128, 128, 1, {w}>"]}
 
@@ -377,7 +375,8 @@ def bench_long(api, la, torch, wl, timer, reps):
     stg = timer.stages(la, lambda: cold.run(), max(3, reps // 2))
     ms_r = timer.cold(lambda: res.run(st), reps)
     med = statistics.median(ms) * 1e-3
-    return {"workload": w.name, "form": la.la_prefill_form(cold.shape), "tokens": N, "heads": H,
+    return {"workload": w.name, "form": la.la_prefill_form(cold.shape),
+            "scan_columns": la.la_prefill_scan_columns(cold.shape, cold.x.cu_host), "tokens": N, "heads": H,
             "cold": dict(summary(ms), tokens_per_s=round(N / med, 1),
                          alg_tflops=round(sum(fl.values()) * N * H / med / 1e12, 2),
                          stage_us={k: round(v * 1e3, 2) for k, v in stg.items()}),
@@ -421,7 +420,8 @@ def bench_tp_rank(api, la, torch, wl, timer, reps):
     warm = statistics.median(timer.warm(step, reps))
     stg = timer.stages(la, step, max(3, reps // 2))
     T = N + (N - B)
-    return {"workload": w.name, "form": la.la_prefill_form(both.shape), "tokens_per_step": T,
+    return {"workload": w.name, "form": la.la_prefill_form(both.shape),
+            "scan_columns": la.la_prefill_scan_columns(both.shape, both.x.cu_host), "tokens_per_step": T,
             "restore_at": B, "step": dict(summary(ms), tokens_per_s=round(T / (statistics.median(ms) * 1e-3), 1)),
             "warm_us": round(warm * 1e3, 2), "stage_us": {k: round(v * 1e3, 2) for k, v in stg.items()}}
 
@@ -578,13 +578,12 @@ def roofline_of(v, la, stages, dk, dv, tokens):
     """The dominant stage of the call and its fraction of the bf16 MFMA peak
     (algorithmic flops) and of the HBM peak (algorithmic bytes)."""
     fl = flops_per_token_head(dk, dv)
-    form = la.la_prefill_form(v.step_call.shape)
     scan_ms = stages["maps_combine"] + stages["scan"]
     dom = "prep" if stages["prep"] > scan_ms else "scan"
     dur = stages["prep"] if dom == "prep" else scan_ms
     flops = fl[dom] * tokens * v.H
     achieved = flops / (dur * 1e-3) / 1e12
-    fk = form_kernels(form, len(v.lens) * v.H)
+    fk = form_kernels(la, v.step_call.shape, v.xs.cu_seqlens)
     kernels = fk[dom] if dom == "prep" else fk["maps_combine"] + fk["scan"]
     return {"bound": "mfma", "kernel": " + ".join(kernels), "achieved": round(achieved, 3),
             "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 5),
@@ -768,6 +767,7 @@ def main():
     fl = flops_per_token_head(dk, dv)
     out["timing"]["warm"] = summary(h["warm"])
     out["step_call"] = {"form": la.la_prefill_form(v.step_call.shape),
+                        "scan_columns": la.la_prefill_scan_columns(v.step_call.shape, v.xs.cu_seqlens),
                         "stage_us": {k: round(x * 1e3, 2) for k, x in st.items()},
                         "alg_tflops": round(sum(fl.values()) * T * H / med / 1e12, 3),
                         "frac_bf16_peak": round(sum(fl.values()) * T * H / med / 1e12 / BF16_PEAK_TFLOPS, 5),
@@ -783,7 +783,8 @@ def main():
                              tokens_per_s=round(TC / (statistics.median(cm) * 1e-3), 1),
                              alg_tflops=round(sum(fl.values()) * TC * H / (statistics.median(cm) * 1e-3) / 1e12, 2),
                              stage_us={k: round(x * 1e3, 2) for k, x in h["cold_stages"].items()},
-                             ckpt_pages_written=v.cold_pages)
+                             ckpt_pages_written=v.cold_pages,
+                             scan_columns=la.la_prefill_scan_columns(v.cold.shape, v.x.cu_seqlens))
     if not args.no_extras:
         reps = max(10, args.steps // 2)
         out["long_prefill"] = bench_long(api, la, torch, wl, timer, reps)

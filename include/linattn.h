@@ -197,6 +197,19 @@ typedef enum la_form {
 la_form la_prefill_form(const la_shape *shape);
 
 /*
+ * la_prefill_scan_columns - state columns per workgroup of the fused scan
+ * that a bf16 prefill call of this shape and these sequence lengths runs
+ * (the single-level scan, or the replay of the two-level form): 32, 64 or
+ * 128.  The width is a scheduling choice made from the chains' chunk
+ * counts (narrow workgroups shorten each chunk's step when few chains
+ * occupy the device); every column's arithmetic is the same at all widths,
+ * so no result depends on it.  cu_seqlens_host: n_seqs + 1 prefix offsets,
+ * as for la_prefill.  Returns 0 for fp32, an invalid or unsupported shape,
+ * or invalid offsets.  Host only; reads nothing but its arguments.
+ */
+int la_prefill_scan_columns(const la_shape *shape, const int32_t *cu_seqlens_host);
+
+/*
  * la_prefill_paged - a prefill (cold or resumed) whose checkpoints go
  * straight into pool pages and whose starting states come straight from pool
  * pages: the save of section 3.1 and the restore of a reload (sections 3.2

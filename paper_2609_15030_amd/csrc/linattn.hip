@@ -287,12 +287,12 @@ double scan_span(const int64_t *nch, int64_t n, int np, double step) {
     return span;
 }
 
-// Column width of the single-level fused scan (bf16, dk = dv = 128) for a
-// call: 128 columns when the chains give every CU two workgroups, else the
-// narrower of 32 and 64 columns whose estimated span is shorter.  Other
-// head sizes take 64.  The width never changes a result.
-int fused_scan_width(const PrefillCall &c) {
-    const la_shape *s = c.shape;
+// Column width of the single-level fused scan for a bf16 call with these
+// sequence lengths (cu_host valid): at dk = dv = 128, 128 columns when the
+// chains give every CU two workgroups, else the narrower of 32 and 64
+// columns whose estimated span is shorter; 64 at other head sizes.  The
+// width never changes a result.
+int fused_scan_width(const la_shape *s, const int32_t *cu_host) {
     const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
     if (s->dk != 128 || s->dv != 128) return 64;
     if (pairs >= 2 * kDeviceCUs) return 128;
@@ -300,19 +300,25 @@ int fused_scan_width(const PrefillCall &c) {
     int64_t nch[2 * kDeviceCUs];
     for (int64_t k = 0; k < pairs; ++k) {
         const int i = (int)(k / s->n_heads);
-        nch[k] = la::n_chunks((int64_t)c.cu_host[i + 1] - c.cu_host[i], s->ckpt_interval, cps);
+        nch[k] = la::n_chunks((int64_t)cu_host[i + 1] - cu_host[i], s->ckpt_interval, cps);
     }
     std::sort(nch, nch + pairs, std::greater<int64_t>());
     return scan_span(nch, pairs, s->dv / 32, kStep32) < scan_span(nch, pairs, s->dv / 64, kStep64) ? 32 : 64;
 }
 
+// Column width of the two-level passes over `units` (sequence, head,
+// segment) units: 128 while that still gives every CU two workgroups (dk =
+// dv = 128), else 64, which spreads each unit over more CUs.
+template <int DK, int DV, int MODE> int two_level_width(int64_t units) {
+    constexpr int NCOLS = MODE == la::kXMap ? DK + DV : DV;
+    return (DK == 128 && DV == 128 && units * (NCOLS / 128) >= 2 * kDeviceCUs) ? 128 : 64;
+}
+
 // The fused scan kernel of one mode over `units` independent units at
-// column width cw (single-level scan), or, for the two-level passes, at the
-// width that still gives every CU two workgroups (128 columns), else at 64
-// columns, which spreads each unit over more CUs.  The width never changes
-// a result: every column's arithmetic is the same at all widths.
+// column width cw (32 for the single-level scan only; 128 at dk = dv = 128
+// only).  Every column's arithmetic is the same at all widths.
 template <int DK, int DV, int MODE>
-la_status launch_xscan(const la::ScanArgs &sa, int64_t units, hipStream_t stream, const char *what, int cw = 0) {
+la_status launch_xscan(const la::ScanArgs &sa, int64_t units, hipStream_t stream, const char *what, int cw) {
     constexpr int NCOLS = MODE == la::kXMap ? DK + DV : DV;
     auto go = [&](auto width) {
         constexpr int CW = decltype(width)::value;
@@ -325,8 +331,7 @@ la_status launch_xscan(const la::ScanArgs &sa, int64_t units, hipStream_t stream
         if constexpr (MODE == la::kXScan) {
             if (cw == 32) return go(std::integral_constant<int, 32>{});
         }
-        if (cw == 128 || (cw == 0 && units * (NCOLS / 128) >= 2 * kDeviceCUs))
-            return go(std::integral_constant<int, 128>{});
+        if (cw == 128) return go(std::integral_constant<int, 128>{});
     }
     return go(std::integral_constant<int, 64>{});
 }
@@ -362,18 +367,21 @@ la_status launch_fused(const PrefillCall &c, const WsPlan &p, int64_t max_chunks
         sa.seg.state = (float *)(base + p.segst);
         const int64_t units = pairs * sa.max_seg;
         if (units > 0)
-            if (la_status e = launch_xscan<DK, DV, la::kXMap>(sa, units, c.stream, "segment map launch")) return e;
+            if (la_status e = launch_xscan<DK, DV, la::kXMap>(sa, units, c.stream, "segment map launch",
+                                                              two_level_width<DK, DV, la::kXMap>(units)))
+                return e;
         hipLaunchKernelGGL((la::gdr_xcombine_kernel<DK, DV>), dim3((unsigned)(8 * (DV / 16) * ((pairs + 7) / 8))),
                            dim3(64), 0, c.stream, sa);
         if (la_status e = hip_check("segment combine launch")) return e;
         trace_mark(2, c.stream);
         if (units > 0)
-            if (la_status e = launch_xscan<DK, DV, la::kXReplay>(sa, units, c.stream, "segment replay launch"))
+            if (la_status e = launch_xscan<DK, DV, la::kXReplay>(sa, units, c.stream, "segment replay launch",
+                                                                 two_level_width<DK, DV, la::kXReplay>(units)))
                 return e;
     } else {
         trace_mark(2, c.stream);
         if (la_status e = launch_xscan<DK, DV, la::kXScan>(sa, pairs, c.stream, "fused scan launch",
-                                                           fused_scan_width(c)))
+                                                           fused_scan_width(s, c.cu_host)))
             return e;
     }
     trace_mark(3, c.stream);
@@ -751,6 +759,22 @@ size_t la_prefill_workspace_bytes(const la_shape *shape, int64_t total_tokens) {
 la_form la_prefill_form(const la_shape *shape) {
     if (check_shape(shape) != LA_OK) return LA_FORM_NONE;
     return prefill_form(shape);
+}
+
+int la_prefill_scan_columns(const la_shape *shape, const int32_t *cu_seqlens_host) {
+    if (check_shape(shape) != LA_OK || shape->io_dtype != LA_BF16 || !cu_seqlens_host || cu_seqlens_host[0] != 0)
+        return 0;
+    const int cps = la::chunks_per_interval(shape->ckpt_interval);
+    int64_t max_chunks = 0;
+    for (int i = 0; i < shape->n_seqs; ++i) {
+        const int64_t len = (int64_t)cu_seqlens_host[i + 1] - cu_seqlens_host[i];
+        if (len < 0 || cu_seqlens_host[i + 1] < 0) return 0;
+        max_chunks = std::max(max_chunks, la::n_chunks(len, shape->ckpt_interval, cps));
+    }
+    if (prefill_form(shape) == LA_FORM_FUSED_SCAN) return fused_scan_width(shape, cu_seqlens_host);
+    const int64_t units = (int64_t)shape->n_seqs * shape->n_heads * ((max_chunks + seg_chunks(shape) - 1) / seg_chunks(shape));
+    return (shape->dk == 128 && shape->dv == 128) ? two_level_width<128, 128, la::kXReplay>(units)
+                                                  : two_level_width<64, 64, la::kXReplay>(units);
 }
 
 la_status la_checkpoint_rows(int32_t n_seqs, const int32_t *cu_seqlens_host, const int64_t *start_pos_host,

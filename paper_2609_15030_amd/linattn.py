@@ -32,7 +32,8 @@ LA_GDR_LITERAL = 0
 LA_GDR_DECAYED_DELTA = 1
 
 EXPORTED = ("strict_prefix_boundary", "la_prefill_workspace_bytes", "la_prefill",
-            "la_prefill_resume", "la_checkpoint_rows", "la_prefill_form", "la_prefill_paged", "la_prefill_paged_noalloc", "la_decode_step", "la_state_save_paged",
+            "la_prefill_resume", "la_checkpoint_rows", "la_prefill_form", "la_prefill_scan_columns",
+            "la_prefill_paged", "la_prefill_paged_noalloc", "la_decode_step", "la_state_save_paged",
             "la_state_restore_paged",
             "la_state_save_host", "la_state_restore_host", "la_hybrid_boundary", "la_hybrid_restore",
             "la_status_string", "la_last_error_message", "la_trace_set_events")
@@ -89,6 +90,7 @@ def _load() -> ctypes.CDLL:
         "la_prefill_resume": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_checkpoint_rows": ([I32, P, P, I64, P, ctypes.POINTER(I64)], I32),
         "la_prefill_form": ([SH], I32),
+        "la_prefill_scan_columns": ([SH, P], I32),
         "la_prefill_paged": ([SH, ctypes.POINTER(LaPages), P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_prefill_paged_noalloc": ([SH, ctypes.POINTER(LaPages), P, P, P, P, P, P, P, P, P, P, P, P, P, P], I32),
         "la_decode_step": ([SH, P, P, P, P, P, P, P, P], I32),
@@ -242,6 +244,13 @@ LA_FORM_NONE, LA_FORM_FUSED_SCAN, LA_FORM_FUSED_TWO_LEVEL, LA_FORM_TILE_SCAN_OUT
 def la_prefill_form(shape: LaShape) -> int:
     """Which kernels a prefill of this shape runs (LA_FORM_*)."""
     return _lib.la_prefill_form(ctypes.byref(shape))
+
+
+def la_prefill_scan_columns(shape: LaShape, cu_seqlens_host) -> int:
+    """State columns per workgroup of the fused scan a bf16 call of this
+    shape and these lengths runs (32, 64 or 128; 0 when it runs none)."""
+    cu = np.ascontiguousarray(cu_seqlens_host, dtype=np.int32)
+    return _lib.la_prefill_scan_columns(ctypes.byref(shape), cu.ctypes.data)
 
 
 def la_checkpoint_rows(cu_seqlens_host, start_pos_host, interval: int):

@@ -275,9 +275,46 @@ def test_two_level_head_dims(dk, dv):
     assert torch.equal(r2.o, res.o[s + B:s + lens[i]]) and torch.equal(r2.final_state[0], res.final_state[i])
 
 
+def _concat(parts):
+    cat = lambda f: np.concatenate([getattr(x, f) for x in parts])
+    lens = [x.total_tokens for x in parts]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    return wl.Inputs(cat("q"), cat("k"), cat("v"), cat("g"), cat("beta"), cu, parts[0].io_dtype)
+
+
+def test_three_column_widths_give_the_same_bits():
+    """One 300-token sequence (C = 128: two checkpoints) run in three calls
+    whose chain counts fix the fused scan's width: alone (8 chains, 32-column
+    workgroups), among 32 sequences of its length (256 equal chains, 64
+    columns) and among 64 sequences (512 chains, 128 columns).  Parity with
+    the oracle, and its output, checkpoints and final state equal bit for
+    bit across the three calls."""
+    H, C, L = 8, 128, 300
+    x = wl.random_inputs(641, [L], H, 128, 128, wl.BF16)
+    rng = np.random.default_rng(642)
+    same = wl.random_inputs(643, [L] * 31, H, 128, 128, wl.BF16)
+    mixed = wl.random_inputs(644, [int(n) for n in rng.integers(1, 400, size=63)], H, 128, 128, wl.BF16)
+    runs = []
+    for batch, what in ((x, "alone, 32 columns"), (_concat([same, x]), "256 equal chains, 64 columns"),
+                        (_concat([mixed, x]), "512 chains, 128 columns")):
+        _, res = _run_cold(batch, C)
+        i = batch.n_seqs - 1
+        s, e = int(batch.cu_seqlens[i]), int(batch.cu_seqlens[i + 1])
+        off = int(res.ckpt_offsets[i])
+        runs.append((res.o[s:e], res.final_state[i:i + 1], res.ckpt[off:off + L // C], what))
+    ref = oracle_run(x, interval=C)
+    o_ref, fin_ref, ck_ref = ref
+    o, fin, ck, _ = runs[0]
+    assert out_err(host(o), o_ref, [0, L]) <= TOL[la.LA_BF16]
+    assert state_err(host(fin), fin_ref) <= TOL[la.LA_BF16]
+    assert state_err(host(ck), ck_ref) <= TOL[la.LA_BF16]
+    for o2, fin2, ck2, what in runs[1:]:
+        assert torch.equal(o2, o) and torch.equal(fin2, fin) and torch.equal(ck2, ck), what
+
+
 def test_column_width_does_not_change_bits():
     """64 sequences x 8 heads (512 chains: the fused scan runs 128-column
-    workgroups) against one of them alone (8 chains: 64-column workgroups):
+    workgroups) against one of them alone (8 chains: 32-column workgroups):
     parity with the oracle on every head, and the lone sequence's output,
     checkpoints and final state equal its rows in the batch bit for bit."""
     rng = np.random.default_rng(640)
