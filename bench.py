@@ -226,14 +226,16 @@ def summary(ms):
 
 
 def form_kernels(la, shape, cu_host, max_segments=1):
-    """Kernel names of a bf16 call (dk = dv = 128): the fused scan's width is
-    the library's choice for these lengths; the segment maps of the
-    two-level form take 128 columns while their units give each of the 256
-    CUs two workgroups, else 64."""
-    w = la.la_prefill_scan_columns(shape, cu_host)
+    """Kernel names of a bf16 call (dk = dv = 128): the fused scan's widths
+    are the library's choice for these lengths (a mix of 32 and 64 columns
+    runs as one mixed-width kernel); the segment maps of the two-level form
+    take 128 columns while their units give each of the 256 CUs two
+    workgroups, else 64."""
+    w, narrow = la.la_prefill_scan_columns(shape, cu_host)
     if la.la_prefill_form(shape) == la.LA_FORM_FUSED_SCAN:
-        return {"prep": ["gdr_xprep_kernel<128>"], "maps_combine": [],
-                "scan": [f"gdr_xscan_kernel<128, 128, 0, {w}>"]}
+        mixed = 0 < narrow < shape.n_seqs * shape.n_heads
+        scan = "gdr_xscan_mixed_kernel<128, 128>" if mixed else f"gdr_xscan_kernel<128, 128, 0, {w}>"
+        return {"prep": ["gdr_xprep_kernel<128>"], "maps_combine": [], "scan": [scan]}
     units = shape.n_seqs * shape.n_heads * max_segments
     return {"prep": ["gdr_xprep_kernel<128>"],
             "maps_combine": [f"gdr_xscan_kernel<128, 128, 2, {128 if units * 2 >= 512 else 64}>",

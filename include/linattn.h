@@ -199,15 +199,19 @@ la_form la_prefill_form(const la_shape *shape);
 /*
  * la_prefill_scan_columns - state columns per workgroup of the fused scan
  * that a bf16 prefill call of this shape and these sequence lengths runs
- * (the single-level scan, or the replay of the two-level form): 32, 64 or
- * 128.  The width is a scheduling choice made from the chains' chunk
- * counts (narrow workgroups shorten each chunk's step when few chains
- * occupy the device); every column's arithmetic is the same at all widths,
- * so no result depends on it.  cu_seqlens_host: n_seqs + 1 prefix offsets,
- * as for la_prefill.  Returns 0 for fp32, an invalid or unsupported shape,
- * or invalid offsets.  Host only; reads nothing but its arguments.
+ * (the single-level scan, or the replay of the two-level form).  The width
+ * is a scheduling choice made from the chains' chunk counts: narrow
+ * workgroups shorten each chunk's step, so the longest (sequence, head)
+ * chains may run in 32-column workgroups while the others run in 64-column
+ * ones.  Every column's arithmetic is the same at all widths, so no result
+ * depends on it.  cu_seqlens_host: n_seqs + 1 prefix offsets, as for
+ * la_prefill.  Returns 32, 64 or 128: the width of every chain, or 64 when
+ * the call mixes 32 and 64; narrow_chains_out (may be NULL) receives the
+ * number of chains, the longest, that run at 32 columns.  Returns 0 (and
+ * 0 chains) for fp32, an invalid or unsupported shape, or invalid offsets.
+ * Host only; reads nothing but its arguments.
  */
-int la_prefill_scan_columns(const la_shape *shape, const int32_t *cu_seqlens_host);
+int la_prefill_scan_columns(const la_shape *shape, const int32_t *cu_seqlens_host, int64_t *narrow_chains_out);
 
 /*
  * la_prefill_paged - a prefill (cold or resumed) whose checkpoints go

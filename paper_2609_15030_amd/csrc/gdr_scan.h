@@ -78,6 +78,7 @@ struct ScanArgs {
     const void *q, *k, *v;        // fused scan: the inputs [T, H, dk | dv] (bf16)
     PageIO pg;
     ChainOrder order;
+    int32_t n_narrow;             // mixed-width fused scan: chains (ranked) in 32-column workgroups
 };
 
 // The chain of workgroup rank k (see ChainOrder); -1 past the last chain.

@@ -173,8 +173,14 @@ __device__ inline void store_state_perm(float *dst, const f32x4 (&S)[DK / 16], u
                                                   (32 * (t >> 1) + 4 * (t & 1) + i) * DV * (int)sizeof(float), 0);
 }
 
+template <int DK, int CW, int MODE>
+using XLdsOf = XLds<DK, CW, MODE != kXMap, xscan_loaders(CW, MODE) ? 2 : 1>;
+
+// One workgroup of the fused scan: block b of this width's blocks, whose
+// units are ranked chains chain0, chain0 + 1, ... (single-level scan) or
+// (sequence, head, segment) units.
 template <int DK, int DV, int MODE, int CW>
-__global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(ScanArgs a) {
+__device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MODE> &sm, int b, int chain0) {
     using M = MT<__bf16>;
     typedef __bf16 T;
     static_assert(CW == 32 || CW == 64 || CW == 128, "column width");
@@ -189,9 +195,8 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
     constexpr int NP = NCOLS / CW;                     // parts per (sequence, head[, segment])
     static_assert(NP * CW == NCOLS && (MODE != kXMap || DK % CW == 0), "column parts");
     constexpr int NVB = kLoad3 ? 2 : 1;                // value buffers
-    using Lds = XLds<DK, CW, kOut, NVB>;
+    using Lds = XLdsOf<DK, CW, MODE>;
     constexpr int KV = Lds::KV;
-    __shared__ Lds sm;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -204,8 +209,8 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
     // ---- unit: (sequence, head[, segment], part); the parts of one chain
     // (or segment) share an XCD and its L2
     int pair, sg = 0;
-    const int b = blockIdx.x, xcd = b & 7, qb = b >> 3;
-    const int part = qb % NP, chain = xcd + 8 * (qb / NP);
+    const int xcd = b & 7, qb = b >> 3;
+    const int part = qb % NP, chain = chain0 + xcd + 8 * (qb / NP);
     if constexpr (MODE == kXScan) {
         pair = chain_of_rank(a, chain);
         if (pair < 0) return;
@@ -711,6 +716,29 @@ __global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(Sc
             xbar_lds();   // C_jj
         }
     }
+}
+
+template <int DK, int DV, int MODE, int CW>
+__global__ __launch_bounds__((xscan_threads(CW, MODE))) void gdr_xscan_kernel(ScanArgs a) {
+    __shared__ XLdsOf<DK, CW, MODE> sm;
+    xscan_block<DK, DV, MODE, CW>(a, sm, blockIdx.x, 0);
+}
+
+// Single-level scan at two widths in one launch: the a.n_narrow longest
+// ranked chains (a multiple of 8) in 32-column workgroups (blocks first),
+// the others in 64-column workgroups.  Both forms have 384 threads and
+// share one LDS allocation.
+template <int DK, int DV>
+__global__ __launch_bounds__(384) void gdr_xscan_mixed_kernel(ScanArgs a) {
+    using L32 = XLdsOf<DK, 32, kXScan>;
+    using L64 = XLdsOf<DK, 64, kXScan>;
+    static_assert(xscan_threads(32, kXScan) == 384 && xscan_threads(64, kXScan) == 384, "one block size");
+    __shared__ __attribute__((aligned(16))) unsigned char raw[sizeof(L32) > sizeof(L64) ? sizeof(L32) : sizeof(L64)];
+    const int nb32 = 4 * a.n_narrow;   // 8 * (DV / 32) blocks per 8 chains
+    if ((int)blockIdx.x < nb32)
+        xscan_block<DK, DV, kXScan, 32>(a, *reinterpret_cast<L32 *>(raw), blockIdx.x, 0);
+    else
+        xscan_block<DK, DV, kXScan, 64>(a, *reinterpret_cast<L64 *>(raw), blockIdx.x - nb32, a.n_narrow);
 }
 
 // Two-level scan, second level: per (sequence, head, 16-column tile), the

@@ -260,50 +260,59 @@ la::ScanArgs scan_args(const PrefillCall &c, const la::Workspace &ws) {
 }
 
 // Per-chunk step of one fused-scan workgroup by column width, relative to
-// the 64-column form's (measured on the MI355X at dk = dv = 128): narrower
-// workgroups give each wave fewer columns, so a chunk takes less time, but
-// a chain then needs more workgroups.
+// the 64-column form's (measured on the MI355X at dk = dv = 128, all CUs
+// busy): narrower workgroups give each wave fewer columns, so a chunk takes
+// less time, but a chain then needs more workgroups.
 constexpr double kStep32 = 0.87, kStep64 = 1.0;
 
-// Estimated span of a fused scan whose n chains have nch[0] >= nch[1] >=
-// ... chunks, np workgroups per chain, each holding a CU of its own (their
-// LDS allows one per CU) for its chain's chunks at `step` per chunk: the
-// workgroups dispatch in that order, each onto the first CU to come free.
-double scan_span(const int64_t *nch, int64_t n, int np, double step) {
-    double free_at[kDeviceCUs];   // min-heap of the CUs' free times
-    int64_t used = 0;
-    double span = 0.0;
-    for (int64_t i = 0; i < n; ++i)
-        for (int p = 0; p < np; ++p) {
-            double t = (double)nch[i] * step;
-            if (used == kDeviceCUs) {
-                std::pop_heap(free_at, free_at + used, std::greater<double>());
-                t += free_at[--used];
-            }
-            free_at[used++] = t;
-            std::push_heap(free_at, free_at + used, std::greater<double>());
-            span = std::max(span, t);
-        }
-    return span;
-}
-
-// Column width of the single-level fused scan for a bf16 call with these
-// sequence lengths (cu_host valid): at dk = dv = 128, 128 columns when the
-// chains give every CU two workgroups, else the narrower of 32 and 64
-// columns whose estimated span is shorter; 64 at other head sizes.  The
-// width never changes a result.
-int fused_scan_width(const la_shape *s, const int32_t *cu_host) {
+// Widths of the single-level fused scan for a bf16 call with these
+// sequence lengths (cu_host valid).  At dk = dv = 128: 128 columns when the
+// chains give every CU two workgroups; else the n_narrow longest chains (a
+// multiple of 8, or all) take 32-column workgroups and the others 64, with
+// n_narrow minimising an estimate of the scan's span: the longest narrow
+// chain, the longest wide chain, or all chunk steps spread over the CUs,
+// whichever is longest (a narrow chain runs four workgroups at kStep32 per
+// chunk, a wide one two at kStep64).  Other head sizes take 64 columns.
+// The widths never change a result.
+struct ScanWidths {
+    int cw;             // 32, 64 or 128; 0 for a mix of 32 (the first n_narrow ranked chains) and 64
+    int64_t n_narrow;
+};
+ScanWidths fused_scan_widths(const la_shape *s, const int32_t *cu_host) {
     const int64_t pairs = (int64_t)s->n_seqs * s->n_heads;
-    if (s->dk != 128 || s->dv != 128) return 64;
-    if (pairs >= 2 * kDeviceCUs) return 128;
+    if (s->dk != 128 || s->dv != 128) return {64, 0};
+    if (pairs >= 2 * kDeviceCUs) return {128, 0};
     const int cps = la::chunks_per_interval(s->ckpt_interval);
     int64_t nch[2 * kDeviceCUs];
+    double total = 0.0;
     for (int64_t k = 0; k < pairs; ++k) {
         const int i = (int)(k / s->n_heads);
         nch[k] = la::n_chunks((int64_t)cu_host[i + 1] - cu_host[i], s->ckpt_interval, cps);
+        total += (double)nch[k];
     }
+    // ranked as the dispatch ranks them (longest first; mixing needs that ranking)
     std::sort(nch, nch + pairs, std::greater<int64_t>());
-    return scan_span(nch, pairs, s->dv / 32, kStep32) < scan_span(nch, pairs, s->dv / 64, kStep64) ? 32 : 64;
+    const bool can_mix = s->n_seqs >= 2 && pairs <= la::kChainOrderMax;
+    double narrow_sum = 0.0, best = 0.0;
+    int64_t best_k = 0, done = 0;
+    auto consider = [&](int64_t k) {
+        for (; done < k; ++done) narrow_sum += (double)nch[done];
+        const double span = std::max({k > 0 ? kStep32 * (double)nch[0] : 0.0,
+                                      k < pairs ? kStep64 * (double)nch[k] : 0.0,
+                                      (4.0 * kStep32 * narrow_sum + 2.0 * kStep64 * (total - narrow_sum)) /
+                                          (double)kDeviceCUs});
+        if (k == 0 || span < best) {
+            best = span;
+            best_k = k;
+        }
+    };
+    consider(0);
+    if (can_mix)
+        for (int64_t k = 8; k < pairs; k += 8) consider(k);
+    consider(pairs);
+    if (best_k == 0) return {64, 0};
+    if (best_k == pairs) return {32, pairs};
+    return {0, best_k};
 }
 
 // Column width of the two-level passes over `units` (sequence, head,
@@ -380,9 +389,16 @@ la_status launch_fused(const PrefillCall &c, const WsPlan &p, int64_t max_chunks
                 return e;
     } else {
         trace_mark(2, c.stream);
-        if (la_status e = launch_xscan<DK, DV, la::kXScan>(sa, pairs, c.stream, "fused scan launch",
-                                                           fused_scan_width(s, c.cu_host)))
-            return e;
+        const ScanWidths sw = fused_scan_widths(s, c.cu_host);
+        if (sw.cw != 0) {
+            if (la_status e = launch_xscan<DK, DV, la::kXScan>(sa, pairs, c.stream, "fused scan launch", sw.cw))
+                return e;
+        } else if constexpr (DK == 128 && DV == 128) {
+            sa.n_narrow = (int32_t)sw.n_narrow;
+            const int64_t blocks = 4 * sw.n_narrow + 16 * ((pairs - sw.n_narrow + 7) / 8);
+            hipLaunchKernelGGL((la::gdr_xscan_mixed_kernel<DK, DV>), dim3((unsigned)blocks), dim3(384), 0, c.stream, sa);
+            if (la_status e = hip_check("fused scan launch")) return e;
+        }
     }
     trace_mark(3, c.stream);
     return LA_OK;
@@ -761,7 +777,8 @@ la_form la_prefill_form(const la_shape *shape) {
     return prefill_form(shape);
 }
 
-int la_prefill_scan_columns(const la_shape *shape, const int32_t *cu_seqlens_host) {
+int la_prefill_scan_columns(const la_shape *shape, const int32_t *cu_seqlens_host, int64_t *narrow_chains_out) {
+    if (narrow_chains_out) *narrow_chains_out = 0;
     if (check_shape(shape) != LA_OK || shape->io_dtype != LA_BF16 || !cu_seqlens_host || cu_seqlens_host[0] != 0)
         return 0;
     const int cps = la::chunks_per_interval(shape->ckpt_interval);
@@ -771,7 +788,11 @@ int la_prefill_scan_columns(const la_shape *shape, const int32_t *cu_seqlens_hos
         if (len < 0 || cu_seqlens_host[i + 1] < 0) return 0;
         max_chunks = std::max(max_chunks, la::n_chunks(len, shape->ckpt_interval, cps));
     }
-    if (prefill_form(shape) == LA_FORM_FUSED_SCAN) return fused_scan_width(shape, cu_seqlens_host);
+    if (prefill_form(shape) == LA_FORM_FUSED_SCAN) {
+        const ScanWidths sw = fused_scan_widths(shape, cu_seqlens_host);
+        if (narrow_chains_out) *narrow_chains_out = sw.cw == 32 ? (int64_t)shape->n_seqs * shape->n_heads : sw.n_narrow;
+        return sw.cw == 0 ? 64 : sw.cw;
+    }
     const int64_t units = (int64_t)shape->n_seqs * shape->n_heads * ((max_chunks + seg_chunks(shape) - 1) / seg_chunks(shape));
     return (shape->dk == 128 && shape->dv == 128) ? two_level_width<128, 128, la::kXReplay>(units)
                                                   : two_level_width<64, 64, la::kXReplay>(units);

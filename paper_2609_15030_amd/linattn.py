@@ -90,7 +90,7 @@ def _load() -> ctypes.CDLL:
         "la_prefill_resume": ([SH, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_checkpoint_rows": ([I32, P, P, I64, P, ctypes.POINTER(I64)], I32),
         "la_prefill_form": ([SH], I32),
-        "la_prefill_scan_columns": ([SH, P], I32),
+        "la_prefill_scan_columns": ([SH, P, ctypes.POINTER(I64)], I32),
         "la_prefill_paged": ([SH, ctypes.POINTER(LaPages), P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P], I32),
         "la_prefill_paged_noalloc": ([SH, ctypes.POINTER(LaPages), P, P, P, P, P, P, P, P, P, P, P, P, P, P], I32),
         "la_decode_step": ([SH, P, P, P, P, P, P, P, P], I32),
@@ -246,11 +246,15 @@ def la_prefill_form(shape: LaShape) -> int:
     return _lib.la_prefill_form(ctypes.byref(shape))
 
 
-def la_prefill_scan_columns(shape: LaShape, cu_seqlens_host) -> int:
-    """State columns per workgroup of the fused scan a bf16 call of this
-    shape and these lengths runs (32, 64 or 128; 0 when it runs none)."""
+def la_prefill_scan_columns(shape: LaShape, cu_seqlens_host):
+    """(columns, narrow chains): the fused scan's workgroup width for a bf16
+    call of this shape and these lengths (32, 64 or 128; 64 for a mix of 32
+    and 64; 0 when it runs none) and how many chains, the longest, run at 32
+    columns."""
     cu = np.ascontiguousarray(cu_seqlens_host, dtype=np.int32)
-    return _lib.la_prefill_scan_columns(ctypes.byref(shape), cu.ctypes.data)
+    narrow = ctypes.c_int64(0)
+    w = _lib.la_prefill_scan_columns(ctypes.byref(shape), cu.ctypes.data, ctypes.byref(narrow))
+    return w, int(narrow.value)
 
 
 def la_checkpoint_rows(cu_seqlens_host, start_pos_host, interval: int):

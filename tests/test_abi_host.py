@@ -165,35 +165,40 @@ def test_prefill_form_is_a_function_of_the_shape():
 
 
 def test_scan_columns_follow_the_chain_counts():
-    """The fused scan's column width is a scheduling choice made from the
+    """The fused scan's column widths are a scheduling choice made from the
     chains' chunk counts: 128 columns once the chains give every CU two
-    workgroups, else 32 when few or uneven chains leave CUs idle (one
-    sequence; a batch whose longest chain dominates) and 64 when the chains
-    are many and even.  fp32 runs no fused scan (0), nor does an invalid
-    call."""
+    workgroups; else the longest chains (a multiple of 8, or all) at 32
+    columns and the rest at 64, as many narrow as shortens the estimated
+    span: all of one sequence's chains, none of many even ones, the longest
+    sequences of a batch whose longest chains dominate.  The call reports
+    (width, narrow chains), with 64 for a mix.  fp32 runs no fused scan
+    (0), nor does an invalid call."""
     W = la.la_prefill_scan_columns
     cu = lambda lens: np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
     sh = lambda n, H=8, C=256, io=la.LA_BF16, d=128: la.make_shape(n, H, d, d, C, io)
-    assert W(sh(1), cu([3584])) == 32                         # one TP rank's 8 chains
-    assert W(sh(32), cu([3584] * 32)) == 64                   # 256 even chains
-    assert W(sh(64), cu([300] * 64)) == 128                   # 512 chains
-    # a batch whose longest sequence is about three times the mean (the
-    # strict-prefix suffixes of the 16-sequence varlen step) against the
-    # same batch all cold (longest about 1.7 times the mean)
+    assert W(sh(1), cu([3584])) == (32, 8)                    # one TP rank's 8 chains
+    assert W(sh(32), cu([3584] * 32)) == (64, 0)              # 256 even chains
+    assert W(sh(64), cu([300] * 64)) == (128, 0)              # 512 chains
+    # the strict-prefix suffixes of the 16-sequence varlen step, and the
+    # same batch all cold: the two (four) longest sequences run narrow
     step = [8064, 7760, 6080, 5136, 4096, 4000, 3840, 3136, 1632, 1504, 960, 368, 240, 176, 176, 80]
     cold = [7760, 8016, 5376, 8064, 3136, 4000, 2656, 5136, 6080, 6320, 4096, 1216, 3696, 7152, 1968, 2784]
-    assert W(sh(16), cu(step)) == 32
-    assert W(sh(16), cu(cold)) == 64
+    assert W(sh(16), cu(step)) == (64, 16)
+    assert W(sh(16), cu(cold)) == (64, 32)
     # the two-level form's replay: (sequence, head, segment) units
-    assert W(sh(1, 16, 1024), cu([32768])) == 128             # 16 x 32 segments
-    assert W(sh(1, 8, 1792), cu([3584])) == 64                # 8 x 2 segments
-    for lens in ([1], [0, 5], [64] * 7):                       # any single-level width is one of three
-        assert W(sh(len(lens), 3, 64), cu(lens)) in (32, 64, 128)
-    assert W(sh(1, d=64), cu([3584])) == 64                    # other head sizes: 64 only
-    assert W(sh(1, io=la.LA_F32), cu([3584])) == 0
-    assert W(la.make_shape(1, 1, 96, 128, 16), cu([10])) == 0
-    assert W(sh(2), np.array([0, 10, 5], np.int32)) == 0       # decreasing offsets
-    assert W(sh(1), np.array([3, 10], np.int32)) == 0          # offsets must start at 0
+    assert W(sh(1, 16, 1024), cu([32768])) == (128, 0)        # 16 x 32 segments
+    assert W(sh(1, 8, 1792), cu([3584])) == (64, 0)           # 8 x 2 segments
+    rng = np.random.default_rng(9)
+    for _ in range(50):                                        # narrow chains: none, all, or a multiple of 8
+        n, H = int(rng.integers(1, 40)), int(rng.integers(1, 12))
+        w, k = W(sh(n, H, 64), cu(rng.integers(0, 3000, n)))
+        assert w in (32, 64, 128) and (k == n * H if w == 32 else (k % 8 == 0 and k < n * H))
+        assert w != 128 or (k == 0 and n * H >= 512)
+    assert W(sh(1, d=64), cu([3584])) == (64, 0)               # other head sizes: 64 only
+    assert W(sh(1, io=la.LA_F32), cu([3584])) == (0, 0)
+    assert W(la.make_shape(1, 1, 96, 128, 16), cu([10])) == (0, 0)
+    assert W(sh(2), np.array([0, 10, 5], np.int32)) == (0, 0)  # decreasing offsets
+    assert W(sh(1), np.array([3, 10], np.int32)) == (0, 0)     # offsets must start at 0
 
 
 def test_checkpoint_rows_match_absolute_multiples():

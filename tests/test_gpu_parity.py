@@ -276,40 +276,47 @@ def test_two_level_head_dims(dk, dv):
 
 
 def _concat(parts):
+    """The sequences of several packed inputs, in order, as one batch."""
     cat = lambda f: np.concatenate([getattr(x, f) for x in parts])
-    lens = [x.total_tokens for x in parts]
+    lens = np.concatenate([np.diff(x.cu_seqlens) for x in parts])
     cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
     return wl.Inputs(cat("q"), cat("k"), cat("v"), cat("g"), cat("beta"), cu, parts[0].io_dtype)
 
 
-def test_three_column_widths_give_the_same_bits():
-    """One 300-token sequence (C = 128: two checkpoints) run in three calls
-    whose chain counts fix the fused scan's width: alone (8 chains, 32-column
-    workgroups), among 32 sequences of its length (256 equal chains, 64
-    columns) and among 64 sequences (512 chains, 128 columns).  Parity with
-    the oracle, and its output, checkpoints and final state equal bit for
-    bit across the three calls."""
+def test_column_widths_give_the_same_bits():
+    """One 300-token sequence (C = 128: two checkpoints) run in calls whose
+    chain counts fix the fused scan's widths: alone (8 chains, 32-column
+    workgroups), among 32 sequences of its length (256 even chains, 64
+    columns), among 64 sequences (512 chains, 128 columns), and in two
+    mixed-width launches, once as the longest sequence (its chains at 32
+    columns, the short ones' at 64) and once behind a longer one (its
+    chains at 64).  Parity with the oracle, and its output, checkpoints and
+    final state equal bit for bit across all five calls."""
     H, C, L = 8, 128, 300
     x = wl.random_inputs(641, [L], H, 128, 128, wl.BF16)
     rng = np.random.default_rng(642)
     same = wl.random_inputs(643, [L] * 31, H, 128, 128, wl.BF16)
     mixed = wl.random_inputs(644, [int(n) for n in rng.integers(1, 400, size=63)], H, 128, 128, wl.BF16)
+    short = wl.random_inputs(645, [64] * 15, H, 128, 128, wl.BF16)
+    longer = wl.random_inputs(646, [1000], H, 128, 128, wl.BF16)
+    cases = ((x, (32, 8)), (_concat([same, x]), (64, 0)), (_concat([mixed, x]), (128, 0)),
+             (_concat([short, x]), (64, 8)), (_concat([longer, short, x]), (64, 8)))
     runs = []
-    for batch, what in ((x, "alone, 32 columns"), (_concat([same, x]), "256 equal chains, 64 columns"),
-                        (_concat([mixed, x]), "512 chains, 128 columns")):
+    for batch, widths in cases:
+        shape = la.make_shape(batch.n_seqs, H, 128, 128, C, la.LA_BF16)
+        assert la.la_prefill_scan_columns(shape, batch.cu_seqlens) == widths, widths
         _, res = _run_cold(batch, C)
         i = batch.n_seqs - 1
         s, e = int(batch.cu_seqlens[i]), int(batch.cu_seqlens[i + 1])
         off = int(res.ckpt_offsets[i])
-        runs.append((res.o[s:e], res.final_state[i:i + 1], res.ckpt[off:off + L // C], what))
-    ref = oracle_run(x, interval=C)
-    o_ref, fin_ref, ck_ref = ref
+        runs.append((res.o[s:e], res.final_state[i:i + 1], res.ckpt[off:off + L // C], widths))
+    o_ref, fin_ref, ck_ref = oracle_run(x, interval=C)
     o, fin, ck, _ = runs[0]
     assert out_err(host(o), o_ref, [0, L]) <= TOL[la.LA_BF16]
     assert state_err(host(fin), fin_ref) <= TOL[la.LA_BF16]
     assert state_err(host(ck), ck_ref) <= TOL[la.LA_BF16]
-    for o2, fin2, ck2, what in runs[1:]:
-        assert torch.equal(o2, o) and torch.equal(fin2, fin) and torch.equal(ck2, ck), what
+    for o2, fin2, ck2, widths in runs[1:]:
+        assert torch.equal(o2, o) and torch.equal(fin2, fin) and torch.equal(ck2, ck), widths
 
 
 def test_column_width_does_not_change_bits():
