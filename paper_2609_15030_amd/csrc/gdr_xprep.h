@@ -46,25 +46,34 @@ struct XPrepArgs {
     int32_t chunk_major;
 };
 
+// A and X are unit-lower-triangular: only their ten 16x16 blocks (bi, bj),
+// bj <= bi, are stored, each with a 17-float row pitch (a column read by
+// the fp32 products touches 16 distinct banks).
+constexpr int kTriBlocks = 10, kBlkPitch = 17, kBlkFloats = 16 * kBlkPitch;
+__device__ inline int tri_blk(int bi, int bj) { return bi * (bi + 1) / 2 + bj; }
+
 template <int DK> struct alignas(16) XPrepSmem {
     static constexpr int LDK = DK + 8;          // bf16 row pitch (16-byte aligned rows)
-    static constexpr int LDA = kChunk + 4;      // fp32 row pitch
-    // K (staged row-major, read by the A = K K^T products) is dead once A is
-    // formed; X takes its place.
+    // K (staged row-major, read by the A = K K^T products) is dead once those
+    // products are in registers; the blocks of A and X take its place.  The
+    // small footprint lets seven workgroups share a CU.
     union {
         __bf16 ks[kChunk][LDK];
-        float xm[kChunk][LDA];
+        struct {
+            float a[kTriBlocks * kBlkFloats];   // A (strictly lower)
+            float x[kTriBlocks * kBlkFloats];   // X = (I + A)^{-1}
+        } t;
     };
-    float am[kChunk][LDA];                      // A (strictly lower)
-    float ysc[4][16][17];                       // per-wave 16x16 scratch
     float G2[kChunk], Gp2[kChunk], bs[kChunk];  // log2e-scaled gates, beta
+    __device__ float *ablk(int bi, int bj) { return t.a + tri_blk(bi, bj) * kBlkFloats; }
+    __device__ float *xblk(int bi, int bj) { return t.x + tri_blk(bi, bj) * kBlkFloats; }
 };
 
 template <int DK>
 __global__ __launch_bounds__(256) void gdr_xprep_kernel(XPrepArgs a) {
     using M = MT<__bf16>;
     using Sm = XPrepSmem<DK>;
-    constexpr int KW = M::KW, KSTEP = M::KSTEP, LDA = Sm::LDA;
+    constexpr int KW = M::KW, KSTEP = M::KSTEP, LB = kBlkPitch;
     __shared__ Sm sm;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -147,19 +156,23 @@ __global__ __launch_bounds__(256) void gdr_xprep_kernel(XPrepArgs a) {
         const float4 gprow = *(const float4 *)&sm.Gp2[16 * mt + 4 * g16];
         const float bv[4] = {brow.x, brow.y, brow.z, brow.w};
         const float gv[4] = {gprow.x, gprow.y, gprow.z, gprow.w};
+        float gcol[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) gcol[nt] = sm.G2[16 * nt + c16];
+        __syncthreads();   // every wave's K reads are done: A takes K's LDS
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
             if (nt > mt) continue;   // wave-uniform
-            const float gcol = sm.G2[16 * nt + c16];
+            float *ab = sm.ablk(mt, nt);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int r = 16 * mt + 4 * g16 + i, s = 16 * nt + c16;
-                const float e = __builtin_amdgcn_exp2f(gv[i] - gcol);
-                sm.am[r][s] = (s < r) ? bv[i] * e * acc[nt][i] : 0.f;
+                const float e = __builtin_amdgcn_exp2f(gv[i] - gcol[nt]);
+                ab[(4 * g16 + i) * LB + c16] = (s < r) ? bv[i] * e * acc[nt][i] : 0.f;
             }
         }
     }
-    __syncthreads();   // K is dead from here on: X takes its LDS
+    __syncthreads();
 
     // ---- 4. X = (I + A)^{-1}: diagonal 16-blocks by substitution -------------
     // Wave w inverts block w with all 64 lanes: lane (q, r), q = lane / 16,
@@ -167,43 +180,46 @@ __global__ __launch_bounds__(256) void gdr_xprep_kernel(XPrepArgs a) {
     // inverse.  Each x[r] receives the updates L[r][s] x[s] in the order
     // s = 0, 1, ..., as forward substitution does.
     {
-        const int base = 16 * wave, q = lane >> 4, r = lane & 15;
+        const int q = lane >> 4, r = lane & 15;
+        const float *ab = sm.ablk(wave, wave);
         float L[16];
 #pragma unroll
-        for (int s4 = 0; s4 < 16; s4 += 4) {
-            const float4 v = *(const float4 *)&sm.am[base + r][base + s4];
-            L[s4] = v.x;
-            L[s4 + 1] = v.y;
-            L[s4 + 2] = v.z;
-            L[s4 + 3] = v.w;
-        }
+        for (int s = 0; s < 16; ++s) L[s] = ab[r * LB + s];
         float x[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) x[c] = (r == 4 * q + c) ? 1.f : 0.f;
         subst_all(x, L);
-        *(float4 *)&sm.xm[base + r][base + 4 * q] = make_float4(x[0], x[1], x[2], x[3]);
+        float *xb = sm.xblk(wave, wave);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) xb[r * LB + 4 * q + c] = x[c];
     }
     __syncthreads();
-    // off-diagonal blocks by bands: X_ij = -X_ii sum_{k=j}^{i-1} A_ik X_kj
+    // off-diagonal blocks by bands: X_ij = -X_ii sum_{k=j}^{i-1} A_ik X_kj.
+    // The sum goes through block X_ij itself, which no other wave reads in
+    // this band: the wave writes it, reads it back as the B operand of the
+    // product with X_ii, and overwrites it with the result.
     for (int d = 1; d < 4; ++d) {
         const int bi = d + wave, bj = wave;
         const bool active = bi < 4;
+        float *xij_blk = active ? sm.xblk(bi, bj) : nullptr;
         if (active) {
             f32x4 y = zero4();
-            for (int bk = bj; bk < bi; ++bk)
-                y = mm16_f32(&sm.am[16 * bi][16 * bk], LDA, &sm.xm[16 * bk][16 * bj], LDA, y, lane);
+            for (int bk = bj; bk < bi; ++bk) y = mm16_f32(sm.ablk(bi, bk), LB, sm.xblk(bk, bj), LB, y, lane);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) sm.ysc[wave][4 * g16 + i][c16] = y[i];
+            for (int i = 0; i < 4; ++i) xij_blk[(4 * g16 + i) * LB + c16] = y[i];
         }
-        // ysc[wave] is written and read by this wave alone: its LDS accesses
+        // the block is written and read by this wave alone: its LDS accesses
         // execute in order, so only the compiler needs holding back here
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         if (active) {
-            f32x4 xij = mm16_f32(&sm.xm[16 * bi][16 * bi], LDA, &sm.ysc[wave][0][0], 17, zero4(), lane);
+            f32x4 xij = mm16_f32(sm.xblk(bi, bi), LB, xij_blk, LB, zero4(), lane);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-            for (int i = 0; i < 4; ++i) sm.xm[16 * bi + 4 * g16 + i][16 * bj + c16] = -xij[i];
+            for (int i = 0; i < 4; ++i) xij_blk[(4 * g16 + i) * LB + c16] = -xij[i];
         }
         __syncthreads();
     }
@@ -211,7 +227,7 @@ __global__ __launch_bounds__(256) void gdr_xprep_kernel(XPrepArgs a) {
     // ---- 5. X fragments: row tile mt = wave, k-steps ks <= mt / 2 -------------
     // Lane (g, c) takes row r = 16 mt + c at columns perm_row(8 ks + j, g):
     // two runs of 4, at 16 (2 ks) + 4 g and 16 (2 ks + 1) + 4 g.  Entries
-    // above the diagonal are zeroed here (the LDS there is stale).
+    // above the diagonal are zero (blocks above it are not stored).
     {
         const int mt = wave, r = 16 * mt + c16;
         uint4 *xout = a.misc + sh * kMiscVec;
@@ -219,11 +235,11 @@ __global__ __launch_bounds__(256) void gdr_xprep_kernel(XPrepArgs a) {
             __bf16 v8[8];
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
-                const int s0 = 16 * (2 * ks + half) + 4 * g16;
-                const float4 x4 = *(const float4 *)&sm.xm[r][s0];
-                const float xv[4] = {x4.x, x4.y, x4.z, x4.w};
+                const int bc = 2 * ks + half, s0 = 16 * bc + 4 * g16;
+                const float *xb = bc <= mt ? sm.xblk(mt, bc) : nullptr;   // wave-uniform
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v8[4 * half + e] = (__bf16)(s0 + e <= r ? xv[e] * sm.bs[s0 + e] : 0.f);
+                for (int e = 0; e < 4; ++e)
+                    v8[4 * half + e] = (__bf16)(xb && s0 + e <= r ? xb[c16 * LB + 4 * g16 + e] * sm.bs[s0 + e] : 0.f);
             }
             xout[xfrag_slot(mt, ks) * 64 + lane] = *(const uint4 *)v8;
         }
