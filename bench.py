@@ -626,7 +626,7 @@ def _short(name):
 def _role(kernel, index, count, steps):
     if kernel.startswith("page_save_kernel"):
         return "calibration copy"
-    if kernel.startswith(("gdr_xprep_kernel", "gdr_xscan_kernel", "gdr_xcombine_kernel")):
+    if kernel.startswith(("gdr_xprep_", "gdr_xscan_", "gdr_xcombine_")):
         return "step" if index >= count - steps else "cold run, warmup, check"
     return "other"
 
@@ -670,7 +670,7 @@ def counters_markdown(dirs, steps):
            "| kernel | role | counter | dispatches | mean per dispatch |", "|---|---|---|---|---|"]
     step_vals = {}
     for (c, k), xs in sorted(per.items()):
-        if not k.startswith(("gdr_xprep_kernel", "gdr_xscan_kernel", "gdr_xcombine_kernel")):
+        if not k.startswith(("gdr_xprep_", "gdr_xscan_", "gdr_xcombine_")):
             continue
         sel = xs[len(xs) - steps:] if len(xs) >= steps else xs
         m = statistics.fmean(sel)
@@ -680,7 +680,7 @@ def counters_markdown(dirs, steps):
     stage_of = {"gdr_xprep_kernel": "prep"}
     roles = {}
     for (c, k), m in step_vals.items():
-        if c not in factor or not k.startswith(("gdr_xprep_kernel", "gdr_xscan_kernel", "gdr_xcombine_kernel")):
+        if c not in factor or not k.startswith(("gdr_xprep_", "gdr_xscan_", "gdr_xcombine_")):
             continue
         stage = stage_of.get(k.split("<")[0], "scan")
         key = "read_bytes" if c == "FETCH_SIZE" else "write_bytes"
@@ -699,7 +699,7 @@ def counters_markdown(dirs, steps):
                 "| kernel | trace avg us (step) | executed bf16 MFMA flops (MOPS x 512) | executed TFLOP/s | "
                 "% of 2,500 | MFMA busy fraction |", "|---|---|---|---|---|---|"]
         for k, m in sorted(mops.items()):
-            if not k.startswith(("gdr_xprep_kernel", "gdr_xscan_kernel", "gdr_xcombine_kernel")):
+            if not k.startswith(("gdr_xprep_", "gdr_xscan_", "gdr_xcombine_")):
                 continue
             ds = dur.get(k, [])
             t = statistics.fmean(ds[len(ds) - steps:]) if ds else float("nan")
