@@ -748,13 +748,21 @@ __global__ __launch_bounds__(384) void gdr_xscan_mixed_kernel(ScanArgs a) {
 // segment-entering states it exchanges with the map and the replay; Phi' is
 // row-major [DK][DK].  Writes the checkpoints (segment ends on a multiple of
 // C), the state entering every later segment, and the final state.
+//
+// One wave per 32 state rows (row tiles 2w, 2w + 1): those two tiles of S,
+// in bf16, are exactly k-step w of the B operand of Phi' S, so each wave
+// hands its fragment to the others through LDS (double-buffered by segment
+// parity, one barrier per segment) and computes its own rows of the next
+// state; a segment step is then 2 KS MFMAs per wave instead of RT KS on one.
 template <int DK, int DV>
-__global__ __launch_bounds__(64) void gdr_xcombine_kernel(ScanArgs a) {
+__global__ __launch_bounds__(64 * (DK / 32)) void gdr_xcombine_kernel(ScanArgs a) {
     using M = MT<__bf16>;
     typedef __bf16 T;
-    constexpr int RT = DK / 16, NT = DV / 16, FS = DK / 4, KS = DK / 32;
-    constexpr int kMfmas = RT * KS, kLoads = 1 + RT + RT * KS;
-    const int lane = threadIdx.x, g16 = lane >> 4, c16 = lane & 15;
+    constexpr int RT = DK / 16, NT = DV / 16, KS = DK / 32;
+    constexpr int kMfmas = 2 * KS, kLoads = 1 + 2 + 2 * KS;
+    __shared__ uint4 sbs[2][KS][64];   // the state's B-operand fragments [segment parity][k-step][lane]
+    const int lane = threadIdx.x & 63, g16 = lane >> 4, c16 = lane & 15;
+    const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));   // row tiles 2w, 2w + 1
     const int b = blockIdx.x, xcd = b & 7, q = b >> 3;
     const int pair = chain_of_rank(a, xcd + 8 * (q / NT)), tile = q % NT;
     const int H = a.n_heads;
@@ -765,24 +773,36 @@ __global__ __launch_bounds__(64) void gdr_xcombine_kernel(ScanArgs a) {
     const int nseg = (nch + a.seg_m - 1) / a.seg_m;
     const int64_t sbase = slot_base_dev(cu0, seq, (int64_t)a.C * a.seg_m, a.cps);
     const int col = 16 * tile + c16;
-    f32x4 S[RT];
+    f32x4 S[2];
     {
-        const float *src = start_state(a, seq, h, (size_t)DK * DV, tile == 0);
+        const float *src = start_state(a, seq, h, (size_t)DK * DV, tile == 0 && w == 0);
 #pragma unroll
-        for (int t = 0; t < RT; ++t)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) S[t][i] = src ? src[(size_t)state_row(16 * t + 4 * g16 + i) * DV + col] : 0.f;
+            for (int i = 0; i < 4; ++i)
+                S[u][i] = src ? src[(size_t)state_row(16 * (2 * w + u) + 4 * g16 + i) * DV + col] : 0.f;
     }
     CkptDst ck;
-    ck.init(a, seq, h, len, (size_t)DK * DV, tile == 0);
-    const uint32_t soff = 4u * (uint32_t)(8 * g16 * DV + col);
+    ck.init(a, seq, h, len, (size_t)DK * DV, tile == 0 && w == 0);
+    // the lane's byte offset of its first row (32 w + 8 g) and its column
+    const uint32_t soff = 4u * (uint32_t)((32 * w + 8 * g16) * DV + col);
+    // rows of this wave's tiles, row-major [DK][DV]: 32 w + 8 g + 4 u + i
+    auto store_rows = [&](float *dst) {
+        const auto r = make_rsrc(dst, DK * DV * sizeof(float));
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_int(S[u][i]), r, (int)soff,
+                                                      (4 * u + i) * DV * (int)sizeof(float), 0);
+    };
     __builtin_amdgcn_s_waitcnt(0);
 
     struct Ops {
         float d;
         int ckid;             // page id of the checkpoint this segment would end (paged)
-        f32x4 r[RT];
-        uint4 ph[RT][KS];
+        f32x4 r[2];
+        uint4 ph[2][KS];
     };
     auto load = [&](Ops &o, int sg) {
         const int64_t ssh = (sbase + sg) * H + h;
@@ -790,30 +810,35 @@ __global__ __launch_bounds__(64) void gdr_xcombine_kernel(ScanArgs a) {
         o.d = buf_load4f(make_rsrc(a.seg.d + ssh, sizeof(float)), 0u, 0u);
         const auto rr = make_rsrc(a.seg.r + ssh * DK * DV, DK * DV * sizeof(float));
 #pragma unroll
-        for (int t = 0; t < RT; ++t) {
-            const uint4 x = buf_load16(rr, 16u * lane, 1024u * (tile * RT + t));
-            o.r[t] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
+        for (int u = 0; u < 2; ++u) {
+            const uint4 x = buf_load16(rr, 16u * lane, 1024u * (tile * RT + 2 * w + u));
+            o.r[u] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
         }
         // A operand of Phi' for state tile t: row state_row(16 t + c), dk 32 ks + 8 g .. + 7
         const auto rp = make_rsrc((const T *)a.seg.phi + ssh * DK * DK, DK * DK * sizeof(T));
 #pragma unroll
-        for (int t = 0; t < RT; ++t)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
-                o.ph[t][ks] = buf_load16(rp, (uint32_t)((state_row(16 * t + c16) * DK + 8 * g16) * sizeof(T)),
+                o.ph[u][ks] = buf_load16(rp, (uint32_t)((state_row(16 * (2 * w + u) + c16) * DK + 8 * g16) * sizeof(T)),
                                          (uint32_t)(32 * ks * sizeof(T)));
     };
     auto step = [&](const Ops &o, int sg) {
-        T sb[FS];
+        // this wave's k-step of S as bf16, to every wave
+        T sb[8];
 #pragma unroll
-        for (int f = 0; f < FS; ++f) sb[f] = (T)S[f >> 2][f & 3];
+        for (int f = 0; f < 8; ++f) sb[f] = (T)S[f >> 2][f & 3];
+        sbs[sg & 1][w][lane] = *(const uint4 *)sb;
+        xbar_lds();
+        bf16x8 bf[KS];
 #pragma unroll
-        for (int t = 0; t < RT; ++t) {
-            f32x4 acc = S[t] * o.d + o.r[t];
+        for (int ks = 0; ks < KS; ++ks) bf[ks] = __builtin_bit_cast(bf16x8, sbs[sg & 1][ks][lane]);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                acc = M::mma(__builtin_bit_cast(bf16x8, o.ph[t][ks]), M::pack(&sb[8 * ks]), acc);
-            S[t] = acc;
+        for (int u = 0; u < 2; ++u) {
+            f32x4 acc = S[u] * o.d + o.r[u];
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) acc = M::mma(__builtin_bit_cast(bf16x8, o.ph[u][ks]), bf[ks], acc);
+            S[u] = acc;
         }
 #pragma unroll
         for (int i = 0; i < kMfmas; ++i) {
@@ -823,13 +848,18 @@ __global__ __launch_bounds__(64) void gdr_xcombine_kernel(ScanArgs a) {
         if (kLoads > kMfmas) __builtin_amdgcn_sched_group_barrier(0x020, kLoads - kMfmas, 0);
         int lo, hi;
         chunk_range32(min((sg + 1) * a.seg_m, nch) - 1, len, a.C, a.cps, &lo, &hi);
-        if (sg + 1 < nseg) store_state_c<RT>(a.seg.state + ((sbase + sg + 1) * H + h) * DK * DV, tile, S);
+        if (sg + 1 < nseg) {
+            float4 *st = (float4 *)(a.seg.state + ((sbase + sg + 1) * H + h) * DK * DV);
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                st[(tile * RT + 2 * w + u) * 64 + lane] = make_float4(S[u][0], S[u][1], S[u][2], S[u][3]);
+        }
         if (hi % a.C == 0) {   // checkpoints come in order, one per C-aligned segment end
-            if (float *d = ck.next(o.ckid)) store_state_perm<DK, DV>(d, S, soff);
+            if (float *d = ck.next(o.ckid)) store_rows(d);
         }
     };
     scan_ring<1>(nseg, load, step, (Ops *)nullptr);
-    if (a.final_state) store_state_perm<DK, DV>(a.final_state + (size_t)pair * DK * DV, S, soff);
+    if (a.final_state) store_rows(a.final_state + (size_t)pair * DK * DV);
 }
 
 }  // namespace la

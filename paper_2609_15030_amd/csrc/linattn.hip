@@ -380,7 +380,7 @@ la_status launch_fused(const PrefillCall &c, const WsPlan &p, int64_t max_chunks
                                                               two_level_width<DK, DV, la::kXMap>(units)))
                 return e;
         hipLaunchKernelGGL((la::gdr_xcombine_kernel<DK, DV>), dim3((unsigned)(8 * (DV / 16) * ((pairs + 7) / 8))),
-                           dim3(64), 0, c.stream, sa);
+                           dim3(64 * (DK / 32)), 0, c.stream, sa);
         if (la_status e = hip_check("segment combine launch")) return e;
         trace_mark(2, c.stream);
         if (units > 0)
