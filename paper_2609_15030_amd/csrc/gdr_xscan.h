@@ -310,6 +310,8 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
 
     if (scan_wave) {
         // ================================ scan wave ================================
+        // the chain: ahead of the helper that shares this wave's SIMD
+        __builtin_amdgcn_s_setprio(2);
         f32x4 S[TW][RT];
         if constexpr (MODE == kXMap) {
 #pragma unroll
