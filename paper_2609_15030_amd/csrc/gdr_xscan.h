@@ -28,12 +28,13 @@
 // addresses apply the same permutation.  The state handed to the output wave
 // (S_0 as bf16 B-operand fragments) and U pass through LDS.
 //
-// Loads: the second wave of each pair (the output wave, or in the map a
-// loader wave) stages every chunk's K, Q, values and the preparation's
-// block (X, gates) one chunk ahead: buffer loads into registers while the
-// chunk before is computed, rows past a chunk's end reading as zero through
-// the buffer range, then LDS stores into the other of two buffers.  The scan
-// waves issue no global loads, so no LDS read of theirs waits on one.
+// Loads: a helper wave of each pair (the loader wave in the 32- and
+// 64-column forms with an output, otherwise the pair's second wave) stages
+// every chunk's K, Q, values and the preparation's block (X, gates) ahead:
+// buffer loads into registers while earlier chunks are computed, rows past
+// a chunk's end reading as zero through the buffer range, then LDS stores
+// into the other of two buffers.  The scan waves issue no global loads, so
+// no LDS read of theirs waits on one.
 // (Loads with an LDS destination would save the registers, but every LDS
 // read after them would wait for them to land.)
 //
@@ -236,8 +237,8 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
     const int vcol0 = (MODE == kXMap) ? cb - DK : cb;  // first value (state) column of the part
     const int pcol = vcol0 + PW * pr;                  // first state column of the wave's pair
 
-    // ---- staging of chunk jj's inputs by the helper waves (the output
-    // waves, or in the map loader waves of their own): global loads into
+    // ---- staging of chunk jj's inputs by the helper waves (the loader
+    // waves, or without them the pairs' second waves): global loads into
     // registers (rows past the chunk's end read as zero through the buffer
     // range), then 16-byte LDS stores.  Helper wave p stages a quarter of K,
     // Q and the preparation's block, and pair p's PW value columns.  The scan
