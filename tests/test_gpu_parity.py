@@ -340,3 +340,30 @@ def test_column_width_does_not_change_bits():
         assert torch.equal(alone.o, res.o[s:e]) and torch.equal(alone.final_state[0], res.final_state[i])
         if alone.n_ckpt_rows:
             assert torch.equal(alone.ckpt, res.ckpt[off:off + alone.n_ckpt_rows])
+
+
+@pytest.mark.parametrize("seed", [650, 651, 652, 653, 654, 655])
+def test_random_batches_against_the_oracle_and_alone(seed):
+    """Seeded random batches (2-24 sequences of 0-900 tokens, 1, 3 or 8
+    heads, C in {64, 128, 192, 256}, d = 128 bf16): whatever widths the
+    batch's chains get, every sequence matches the oracle, and a sequence
+    run alone (its own widths) gives the same bits."""
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(2, 25))
+    H = int(rng.choice([1, 3, 8]))
+    C = int(rng.choice([64, 128, 192, 256]))
+    lens = [int(v) for v in rng.integers(0, 901, size=n)]
+    x = wl.random_inputs(seed, lens, H, 128, 128, wl.BF16)
+    shape = la.make_shape(n, H, 128, 128, C, la.LA_BF16)
+    print(f"[parity] seed {seed}: {n} seqs x {H} heads, C={C}, widths "
+          f"{la.la_prefill_scan_columns(shape, x.cu_seqlens)}", flush=True)
+    _, res = _run_cold(x, C)
+    compare(res, oracle_run(x, interval=C), x.cu_seqlens, TOL[la.LA_BF16], f"random batch {seed}")
+    i = int(np.argmax(lens))
+    alone = api.prefill(api.to_device(x.seq(i)), C)
+    torch.cuda.synchronize()
+    s, e = int(x.cu_seqlens[i]), int(x.cu_seqlens[i + 1])
+    off = int(res.ckpt_offsets[i])
+    assert torch.equal(alone.o, res.o[s:e]) and torch.equal(alone.final_state[0], res.final_state[i])
+    if alone.n_ckpt_rows:
+        assert torch.equal(alone.ckpt, res.ckpt[off:off + alone.n_ckpt_rows])
