@@ -428,6 +428,38 @@ def bench_tp_rank(api, la, torch, wl, timer, reps):
             "warm_us": round(warm * 1e3, 2), "stage_us": {k: round(v * 1e3, 2) for k, v in stg.items()}}
 
 
+def bench_sweep(api, la, torch, wl, timer, reps):
+    """The nine-length serial sweep (T = 512 i, 8 heads, d = 128, bf16,
+    C = 256): per length, the cold paged prefill (every checkpoint into its
+    pool page) and the resume of the suffix from the strict-prefix page, each
+    timed on its own after a cache flush; the resume's output is checked
+    against the cold run's suffix, bit for bit."""
+    rows_out = []
+    for w in wl.nine_length_sweep():
+        x, C = w.inputs, w.interval
+        N, H, dk, dv = x.total_tokens, x.n_heads, x.dk, x.dv
+        B = la.strict_prefix_boundary(N, C, w.available[0])
+        cold = api.Prefill(api.to_device(x), C, emit_ckpt=False)
+        res = api.Prefill(api.to_device(x.tokens(B, N)), C, starts=[B], emit_ckpt=False)
+        pool = torch.zeros((cold.n_ckpt_rows * H, dk * dv), dtype=torch.float32, device="cuda")
+        ids = torch.arange(cold.n_ckpt_rows * H, dtype=torch.int32, device="cuda")
+        j = B // C - 1
+        st_ids = ids[j * H:(j + 1) * H].contiguous()
+        ck_ids = ids[(j + 1) * H:(j + 1 + res.n_ckpt_rows) * H].contiguous()
+        run_cold = lambda: cold.run_paged(pool, ckpt_page_ids=ids)
+        run_res = lambda: res.run_paged(pool, ckpt_page_ids=ck_ids, state_page_ids=st_ids)
+        run_cold()
+        run_res()
+        torch.cuda.synchronize()
+        assert torch.equal(res.o, cold.o[B:]) and torch.equal(res.final, cold.final)
+        mc = statistics.median(timer.cold(run_cold, reps))
+        mr = statistics.median(timer.cold(run_res, reps))
+        rows_out.append({"T": N, "restore_at": B, "cold_us": round(mc * 1e3, 2),
+                         "cold_tokens_per_s": round(N / (mc * 1e-3), 1), "resume_us": round(mr * 1e3, 2),
+                         "ckpt_pages": cold.n_ckpt_rows * H})
+    return {"workload": "sweep_T512..4608_H8_d128_bf16_C256", "runs": rows_out}
+
+
 def bench_decode(la, torch, stream_ptr, H, dk, dv, C, batches=(1, 64), steps=200):
     """Decode continuation: one token per (sequence, head) per call, state read
     and written in HBM (2 x 4 dk dv bytes per head-token)."""
@@ -791,6 +823,7 @@ def main():
         reps = max(10, args.steps // 2)
         out["long_prefill"] = bench_long(api, la, torch, wl, timer, reps)
         out["tp_rank"] = bench_tp_rank(api, la, torch, wl, timer, reps)
+        out["sweep"] = bench_sweep(api, la, torch, wl, timer, max(5, reps // 2))
         out["save_restore"] = bench_pool(la, torch, timer)
         out["decode"] = bench_decode(la, torch, sp, H, dk, dv, v.C)
         out["host_tier"] = bench_host_tier(la, torch, timer)
