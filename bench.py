@@ -50,6 +50,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import statistics
 import sys
 import time
@@ -122,10 +123,16 @@ def step_bytes(tokens, heads, dk, dv, n_seqs, ckpt_pages, restored_pages, io=2):
 
 
 def kernel_source_hash():
+    """SHA-256 of the kernel sources with their comments and blank lines
+    removed (a comment edit leaves the recorded counters valid; any change to
+    the code does not)."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        lines = (re.sub(r"//.*$", "", ln).rstrip() for ln in text.splitlines())
+        h.update("\n".join(ln for ln in lines if ln).encode())
     return h.hexdigest()
 
 
