@@ -106,14 +106,20 @@ template <int DK, int CW, bool OUT, int NVB> struct XLds {
 
 // Physical 16-byte piece of logical piece p in row r of a K or Q tile (DK / 8
 // pieces per row): the XOR swizzle spreads the rows of a fragment read over
-// the LDS banks.
-template <int DK> __device__ inline int xpiece(int r, int p) { return p ^ (r & (DK / 8 - 1)); }
+// the LDS banks.  The plain key (r) keeps the 16 rows of a row-fragment read
+// apart; the mixed key (r ^ 4 r, low bits) does too, and also spreads the
+// 4 rows x 4 pieces of a K^T transposed read over 16 pieces where the plain
+// key gives 4.  Measured per kernel: the mixed key speeds up the segment
+// maps (no output waves) and slows the 32-column scan, so only the maps use it.
+template <int DK, bool MIX> __device__ inline int xpiece(int r, int p) {
+    return p ^ ((MIX ? (r ^ (r << 2)) : r) & (DK / 8 - 1));
+}
 
 // A-operand fragment of rows [16 mt, 16 mt + 16) of a K or Q tile, k-step ks
 // (dk 32 ks + 8 g .. + 7): one 16-byte read.
-template <int DK> __device__ inline bf16x8 row_frag(const uint4 *tile, int mt, int ks, int lane) {
+template <int DK, bool MIX> __device__ inline bf16x8 row_frag(const uint4 *tile, int mt, int ks, int lane) {
     const int r = 16 * mt + (lane & 15), g = lane >> 4;
-    return __builtin_bit_cast(bf16x8, tile[r * (DK / 8) + xpiece<DK>(r, 4 * ks + g)]);
+    return __builtin_bit_cast(bf16x8, tile[r * (DK / 8) + xpiece<DK, MIX>(r, 4 * ks + g)]);
 }
 
 // A-operand fragment of K^T for state tile t (rows state_row(16 t + i)) and
@@ -123,7 +129,7 @@ template <int DK> __device__ inline bf16x8 row_frag(const uint4 *tile, int mt, i
 // 4 c + q receives column (that of source lanes c, c + 4, ...) + q of rows
 // base .. base + 3, so reading the 4 columns 32 (t / 2) + 4 (t % 2) + 8 c
 // gives lane 4 c + q exactly state_row(16 t + 4 c + q).
-template <int DK> __device__ inline bf16x8 kt_frag(const uint4 *k, int t, int ks, int lane) {
+template <int DK, bool MIX> __device__ inline bf16x8 kt_frag(const uint4 *k, int t, int ks, int lane) {
     typedef short i16x8 __attribute__((ext_vector_type(8)));
     const int g = lane >> 4, s = lane & 15;
     const int piece = 4 * (t >> 1) + (s & 3), half = 8 * (t & 1);
@@ -131,7 +137,7 @@ template <int DK> __device__ inline bf16x8 kt_frag(const uint4 *k, int t, int ks
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
         const int r = 32 * ks + 16 * u + 4 * g + (s >> 2);
-        const char *p = (const char *)k + (r * (DK / 8) + xpiece<DK>(r, piece)) * 16 + half;
+        const char *p = (const char *)k + (r * (DK / 8) + xpiece<DK, MIX>(r, piece)) * 16 + half;
         h[u] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4 *)p);
     }
     const i16x8 both = {h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
@@ -191,6 +197,7 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
     constexpr int PW = 16 * TW;                        // state columns per pair
     constexpr int NTH = xscan_threads(CW, MODE);
     constexpr bool kLoad3 = xscan_loaders(CW, MODE);   // loader waves of their own
+    constexpr bool kMix = MODE == kXMap;               // K swizzle key (xpiece)
     constexpr int RT = DK / 16, FS = DK / 4, KS = DK / 32;
     constexpr int NCOLS = (MODE == kXMap) ? DK + DV : DV;   // column space of the unit
     constexpr int NP = NCOLS / CW;                     // parts per (sequence, head[, segment])
@@ -290,8 +297,8 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
 #pragma unroll
         for (int it = 0; it < KPW; ++it) {
             const int e = (pr * KPW + it) * 64 + lane, r = e / (DK / 8), p = e % (DK / 8);
-            B.k[r * (DK / 8) + xpiece<DK>(r, p)] = st.k[it];
-            if constexpr (kOut) B.q[r * (DK / 8) + xpiece<DK>(r, p)] = st.q[it];
+            B.k[r * (DK / 8) + xpiece<DK, kMix>(r, p)] = st.k[it];
+            if constexpr (kOut) B.q[r * (DK / 8) + xpiece<DK, kMix>(r, p)] = st.q[it];
         }
 #pragma unroll
         for (int it = 0; it < MPW; ++it) {
@@ -372,13 +379,13 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) kf[mt][ks] = row_frag<DK>(B.k, mt, ks, lane);
+                for (int ks = 0; ks < KS; ++ks) kf[mt][ks] = row_frag<DK, kMix>(B.k, mt, ks, lane);
             const float eL = __builtin_amdgcn_exp2f(gate[kChunk - 1] * kLog2e);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int mt = 2; mt < 4; ++mt)
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) kf[mt][ks] = row_frag<DK>(B.k, mt, ks, lane);
+                for (int ks = 0; ks < KS; ++ks) kf[mt][ks] = row_frag<DK, kMix>(B.k, mt, ks, lane);
             f32x4 Y[TW][4];
 #pragma unroll
             for (int mt = 0; mt < 2; ++mt)
@@ -423,7 +430,7 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
 #pragma unroll
             for (int t = 0; t < RT / 2; ++t)
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) kt[t][ks] = kt_frag<DK>(B.k, t, ks, lane);
+                for (int ks = 0; ks < 2; ++ks) kt[t][ks] = kt_frag<DK, kMix>(B.k, t, ks, lane);
             __builtin_amdgcn_sched_barrier(0);
             // ---- Z = V - diag(exp(Gp)) Y; U = X diag(beta) Z
             T zb[TW][16];
@@ -442,7 +449,7 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
 #pragma unroll
             for (int t = RT / 2; t < RT; ++t)
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) kt[t][ks] = kt_frag<DK>(B.k, t, ks, lane);
+                for (int ks = 0; ks < 2; ++ks) kt[t][ks] = kt_frag<DK, kMix>(B.k, t, ks, lane);
             __builtin_amdgcn_sched_barrier(0);
             f32x4 U[TW][4];
 #pragma unroll
@@ -604,15 +611,15 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) qf[mt][ks] = row_frag<DK>(B.q, mt, ks, lane);
+                    for (int ks = 0; ks < KS; ++ks) qf[mt][ks] = row_frag<DK, kMix>(B.q, mt, ks, lane);
                 // K fragments of this wave's P tiles: column block nt = pr (and
                 // nt = 0 for the tile (3, 0) the last wave takes over)
                 bf16x8 pk[KS], pk0[KS];
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) pk[ks] = row_frag<DK>(B.k, pr, ks, lane);
+                for (int ks = 0; ks < KS; ++ks) pk[ks] = row_frag<DK, kMix>(B.k, pr, ks, lane);
                 if (pr == NPAIR - 1 && NPAIR > 1) {
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) pk0[ks] = row_frag<DK>(B.k, 0, ks, lane);
+                    for (int ks = 0; ks < KS; ++ks) pk0[ks] = row_frag<DK, kMix>(B.k, 0, ks, lane);
                 }
                 __builtin_amdgcn_sched_barrier(0);
                 // ---- S_0^T Q^T
@@ -658,7 +665,7 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
                         for (int mt = 0; mt < 4; ++mt) p_tile(mt, 0, pk, qf[mt]);
                         bf16x8 kk[KS];
 #pragma unroll
-                        for (int ks = 0; ks < KS; ++ks) kk[ks] = row_frag<DK>(B.k, 1, ks, lane);
+                        for (int ks = 0; ks < KS; ++ks) kk[ks] = row_frag<DK, kMix>(B.k, 1, ks, lane);
                         p_tile(1, 1, kk, qf[1]);
                     } else {
 #pragma unroll
@@ -667,7 +674,7 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
                         for (int nt = 2; nt < 4; ++nt) {
                             bf16x8 kk[KS];
 #pragma unroll
-                            for (int ks = 0; ks < KS; ++ks) kk[ks] = row_frag<DK>(B.k, nt, ks, lane);
+                            for (int ks = 0; ks < KS; ++ks) kk[ks] = row_frag<DK, kMix>(B.k, nt, ks, lane);
 #pragma unroll
                             for (int mt = nt; mt < 4; ++mt) p_tile(mt, nt, kk, qf[mt]);
                         }
@@ -692,21 +699,47 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
                 for (int mt = 0; mt < 4; ++mt) eg[mt] = __builtin_amdgcn_exp2f(gate[16 * mt + c16] * kLog2e);
                 __builtin_amdgcn_sched_barrier(0);
                 T *obase = (T *)a.o + (((int64_t)cu0 + lo) * H + h) * DV;
-                const auto ro = make_rsrc(obase, head_rows_bytes<T>(n, H, DV));
+                [[maybe_unused]] const auto ro = make_rsrc(obase, head_rows_bytes<T>(n, H, DV));
 #pragma unroll
-                for (int mt = 0; mt < 4; ++mt)
+                for (int mt = 0; mt < 4; ++mt) {
+                    uint2 out[TW];   // 4 bf16 columns of row 16 mt + c16 per tile
 #pragma unroll
                     for (int c = 0; c < TW; ++c) {
                         f32x4 acc = O[c][mt] * eg[mt];
 #pragma unroll
                         for (int ks = 0; ks <= (mt >> 1); ++ks) acc = M::mma(ubf[c][ks], pfr[xfrag_slot(mt, ks)], acc);
-                        T out[4];
+                        T o4[4];
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) out[e] = (T)(acc[e] * scale);
-                        const uint32_t voff = ((uint32_t)(16 * mt + c16) * (uint32_t)(H * DV) +
-                                               (uint32_t)(pcol + 16 * c + 4 * g16)) * (uint32_t)sizeof(T);
-                        buf_store8(*(const uint2 *)out, ro, voff, 0u);
+                        for (int e = 0; e < 4; ++e) o4[e] = (T)(acc[e] * scale);
+                        out[c] = *(const uint2 *)o4;
                     }
+                    if constexpr (CW == 128) {
+                        // Lane groups g and g ^ 1 trade halves (ds_swizzle, lane ^ 16
+                        // within 32) so that even groups hold 8 consecutive columns of
+                        // tile 0 and odd groups 8 of tile 1: one 16-byte store per lane,
+                        // 64 contiguous bytes per row instead of two 32-byte pieces.
+                        // Without loader waves the output wave's stores queue ahead of
+                        // its next staging loads, so halving them shortens its chunk
+                        // (the 64-column form, whose loaders issue those loads, is
+                        // measured slower with it).
+                        const bool odd = g16 & 1;
+                        const uint2 send = odd ? out[0] : out[1];
+                        const uint2 recv = make_uint2((uint32_t)__builtin_amdgcn_ds_swizzle((int)send.x, 0x401F),
+                                                      (uint32_t)__builtin_amdgcn_ds_swizzle((int)send.y, 0x401F));
+                        const uint4 v = odd ? make_uint4(recv.x, recv.y, out[1].x, out[1].y)
+                                            : make_uint4(out[0].x, out[0].y, recv.x, recv.y);
+                        const int row = 16 * mt + c16;
+                        if (row < n)
+                            *(uint4 *)(obase + (int64_t)row * H * DV + pcol + 16 * (g16 & 1) + 8 * (g16 >> 1)) = v;
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < TW; ++c) {
+                            const uint32_t voff = ((uint32_t)(16 * mt + c16) * (uint32_t)(H * DV) +
+                                                   (uint32_t)(pcol + 16 * c + 4 * g16)) * (uint32_t)sizeof(T);
+                            buf_store8(out[c], ro, voff, 0u);
+                        }
+                    }
+                }
             }
             // chunk jj + 1's inputs: the other buffers were last read in chunk
             // jj - 1
