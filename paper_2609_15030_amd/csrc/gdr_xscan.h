@@ -527,14 +527,20 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
             for (int c = 0; c < TW; ++c) {
                 const int col = cb + PW * pr + 16 * c + c16;
                 if (phi) {
-                    // Phi' = Phi - D I, row-major [DK][DK] in the io type
-                    T *dst = (T *)a.seg.phi + ssh * DK * DK + col;
+                    // Phi' = Phi - D I in the io type, stored as the combine's A-operand
+                    // fragments: [tile t][k-step ks][lane 16 g + c][8], row
+                    // state_row(16 t + c), columns 32 ks + 8 g .. + 7, so that each of
+                    // the combine's fragment loads is 1 KB contiguous.  This lane holds
+                    // rows state_row(16 t + 4 g16 + e) of column col.
+                    T *dst = (T *)a.seg.phi + ssh * DK * DK;
+                    const int fks = col >> 5, fg = (col >> 3) & 3, fj = col & 7;
 #pragma unroll
                     for (int t = 0; t < RT; ++t)
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
                             const int r = state_row(16 * t + 4 * g16 + e);
-                            dst[(size_t)r * DK] = (T)(S[c][t][e] - (r == col ? dprod : 0.f));
+                            dst[((size_t)(t * KS + fks) * 64 + 16 * fg + 4 * g16 + e) * 8 + fj] =
+                                (T)(S[c][t][e] - (r == col ? dprod : 0.f));
                         }
                 } else {
                     float4 *dst = (float4 *)(a.seg.r + ssh * DK * DV);
@@ -782,7 +788,7 @@ __global__ __launch_bounds__(384) void gdr_xscan_mixed_kernel(ScanArgs a) {
 // in fp32; only Phi' S goes through the bf16 MFMA).  The state's rows are
 // held in the fused scan's permutation (state_row), as are R and the
 // segment-entering states it exchanges with the map and the replay; Phi' is
-// row-major [DK][DK].  Writes the checkpoints (segment ends on a multiple of
+// in the A-operand fragment order the map writes.  Writes the checkpoints (segment ends on a multiple of
 // C), the state entering every later segment, and the final state.
 //
 // One wave per 32 state rows (row tiles 2w, 2w + 1): those two tiles of S,
@@ -850,14 +856,14 @@ __global__ __launch_bounds__(64 * (DK / 32)) void gdr_xcombine_kernel(ScanArgs a
             const uint4 x = buf_load16(rr, 16u * lane, 1024u * (tile * RT + 2 * w + u));
             o.r[u] = f32x4{__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
         }
-        // A operand of Phi' for state tile t: row state_row(16 t + c), dk 32 ks + 8 g .. + 7
+        // A operand of Phi' for state tile t (row state_row(16 t + c), dk 32 ks + 8 g .. + 7),
+        // stored by the map in fragment order: one contiguous 1 KB load each
         const auto rp = make_rsrc((const T *)a.seg.phi + ssh * DK * DK, DK * DK * sizeof(T));
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
-                o.ph[u][ks] = buf_load16(rp, (uint32_t)((state_row(16 * (2 * w + u) + c16) * DK + 8 * g16) * sizeof(T)),
-                                         (uint32_t)(32 * ks * sizeof(T)));
+                o.ph[u][ks] = buf_load16(rp, 16u * lane, (uint32_t)(((2 * w + u) * KS + ks) * 1024));
     };
     auto step = [&](const Ops &o, int sg) {
         // this wave's k-step of S as bf16, to every wave
