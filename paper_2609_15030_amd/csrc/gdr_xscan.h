@@ -247,14 +247,21 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
     // ---- staging of chunk jj's inputs by the helper waves (the loader
     // waves, or without them the pairs' second waves): global loads into
     // registers (rows past the chunk's end read as zero through the buffer
-    // range), then 16-byte LDS stores.  Helper wave p stages a quarter of K,
-    // Q and the preparation's block, and pair p's PW value columns.  The scan
+    // range), then 16-byte LDS stores.  Helper wave p stages its share of K,
+    // Q, the preparation's block and the workgroup's CW value columns (those
+    // taken row by row across all pairs, so that each load instruction reads
+    // whole CW-column row pieces rather than one pair's PW columns).  The scan
     // waves issue no global loads, so nothing they read from LDS waits on a
     // load in flight.
     constexpr int KPW = KV / 64 / NPAIR;                 // 16-byte pieces of K per helper lane
     constexpr int MPW = (kMiscVec + 64 * NPAIR - 1) / (64 * NPAIR);
     constexpr int VPR = PW / 8;                          // 16-byte pieces of a value row of a pair
-    constexpr int VPW = kChunk * VPR / 64;               // pieces of a pair's values per lane
+    constexpr int VPC = CW / 8;                          // 16-byte pieces of a value row of the workgroup
+    constexpr int VPW = kChunk * VPC / 64 / NPAIR;       // pieces of the values per helper lane
+    static_assert(VPW * 64 * NPAIR == kChunk * VPC, "value staging tiling");
+    constexpr int VROWS = 64 / VPC, VLP = 64 / NPAIR;    // rows per value load; lanes per pair
+    auto vrow = [&](int it) { return (pr * VPW + it) * VROWS + (lane % VLP) / VPR; };
+    auto vpiece = [&]() { return (lane / VLP) * VPR + lane % VPR; };
     static_assert(KPW * 64 * NPAIR == KV, "K staging tiling");
     struct Stage {
         uint4 k[KPW], q[kOut ? KPW : 1], m[MPW], v[VPW];
@@ -284,11 +291,11 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
         for (int it = 0; it < MPW; ++it)
             st.m[it] = buf_load16(rm, (uint32_t)(((pr * MPW + it) * 64 + lane) * 16), 0u);
         const uint32_t vbytes =
-            (has_v && live) ? (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)((n - 1) * H * DV + PW) * 2)) : 0u;
-        const auto rv = make_rsrc(vin + row0 * DV + pcol, vbytes);
+            (has_v && live) ? (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)((n - 1) * H * DV + CW) * 2)) : 0u;
+        const auto rv = make_rsrc(vin + row0 * DV + vcol0, vbytes);
 #pragma unroll
         for (int it = 0; it < VPW; ++it) {
-            const int e = it * 64 + lane, r = e / VPR, p = e % VPR;
+            const int r = vrow(it), p = vpiece();
             st.v[it] = buf_load16(rv, (uint32_t)(r * H * DV * 2 + 16 * p), 0u);
         }
     };
@@ -306,9 +313,17 @@ __device__ __forceinline__ void xscan_block(const ScanArgs &a, XLdsOf<DK, CW, MO
             if (e < kMiscVec) B.misc[e] = st.m[it];
         }
     };
+    // Each of the helper's value loads covers VROWS whole rows of the
+    // workgroup's CW columns: lane l takes pair l / (64 / NPAIR), so that the
+    // lanes of one pair store a contiguous run of that pair's row-major
+    // [64][PW] block.
     auto stage_store_values = [&](const Stage &st, int bi) {
+        uint4 *vb = &sm.v[bi % NVB][0][0];
 #pragma unroll
-        for (int it = 0; it < VPW; ++it) sm.v[bi % NVB][pr][it * 64 + lane] = st.v[it];
+        for (int it = 0; it < VPW; ++it) {
+            const int r = vrow(it), p = vpiece();
+            vb[(p / VPR) * (kChunk * VPR) + r * VPR + p % VPR] = st.v[it];
+        }
     };
 
     // P fragments above the diagonal that no P tile writes stay zero
